@@ -1,0 +1,198 @@
+#!/usr/bin/env python3
+"""Benchmark of the chunked causal attention hot path on one MI355X.
+
+A step is one forward walk over all chunks (each chunk's Q/K/V/O/LSE
+offloaded to pinned host memory after its forward, except the last chunk)
+followed by the reverse backward walk (offloaded chunks prefetched two
+chunks ahead), on synthetic N(0,1) bf16 inputs already resident in HBM.
+
+Reported (one JSON line):
+  value          algorithmic TFLOP/s of the step with offload on; the
+                 algorithmic count is 14*B*Hq*D per visible (query, key)
+                 pair (forward QK^T, PV; backward the five products), the
+                 causal half only
+  pct_peak       value / 2516.6 TFLOP/s (256 CU x 2.4 GHz x 4096 bf16
+                 flop/clk/CU, dense)
+  offload_hidden 1 - max(0, T_on - T_off) / T_copy, where T_off is the same
+                 step without offload and T_copy the event-timed copy busy
+                 time per step
+  roofline       the dominant kernel (largest summed time), from HIP events
+                 around every launch on the compute stream in the timed steps
+  cpu_baseline   the fp64 oracle on a bounded sample (one head, a prefix of
+                 the sequence), in algorithmic TFLOP/s
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+PEAK_BF16_TFLOPS = 256 * 2.4e9 * 4096 / 1e12  # dense bf16 MFMA, MI355X
+HBM_PEAK_GBS = 8000.0
+METRIC = "chunked causal attn fwd+bwd TFLOP/s (% bf16 MFMA peak) + % offload hidden"
+
+WORKLOADS = {
+    # name: (S, N, Hq, Hkv, D, offload)
+    "s128k_n16_offload": (131072, 16, 32, 32, 128, "qkvol"),
+    "s32k_n8": (32768, 8, 32, 32, 128, "none"),
+    "s512k_n32_gqa_offload": (524288, 32, 32, 8, 128, "qkvol"),
+    "s1m_n64_offload": (1048576, 64, 32, 32, 128, "qkvol"),
+}
+DEFAULT_WORKLOAD = "s128k_n16_offload"
+
+
+def pairs_per_chunk(offsets):
+    """Visible (query, key) pairs of each chunk: s_i * c_i + s_i (s_i + 1) / 2."""
+    out = []
+    for i in range(len(offsets) - 1):
+        c, s = offsets[i], offsets[i + 1] - offsets[i]
+        out.append(s * c + s * (s + 1) // 2)
+    return out
+
+
+def algorithmic_flops(offsets, B, Hq, D):
+    """Per kernel, summed over chunks: fwd 4D, dkdv 8D (S, dP, dV, dK), dq 2D
+    (dQ; its S/dP recomputation is not credited) per visible pair and head."""
+    p = sum(pairs_per_chunk(offsets)) * B * Hq * D
+    return {"fwd": 4 * p, "bwd_dkdv": 8 * p, "bwd_dq": 2 * p, "bwd_pre": 0, "total": 14 * p}
+
+
+def oracle_cpu_baseline(inp, D, sample_tokens):
+    """Time the fp64 oracle (fwd + bwd, unchunked) on head 0 of the first
+    ``sample_tokens`` tokens of the same inputs."""
+    import numpy as np
+
+    import oracle
+
+    def host(t, h):
+        return t[:, :sample_tokens, h:h + 1].float().cpu().numpy().astype(np.float64)
+
+    q, k, v, do = host(inp["q"], 0), host(inp["k"], 0), host(inp["v"], 0), host(inp["do"], 0)
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max(i.get("num_threads", 1) for i in threadpool_info()) if threadpool_info() else 1
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    t0 = time.perf_counter()
+    oracle.attention(q, k, v, do, 1.0 / math.sqrt(D))
+    dt = time.perf_counter() - t0
+    flops = 14 * D * sample_tokens * (sample_tokens + 1) / 2
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"fp64 NumPy oracle, unchunked fwd+bwd of head 0 over the first {sample_tokens} "
+                      f"tokens ({flops:.3e} algorithmic flop in {dt:.2f} s)",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
+    ap.add_argument("--lookahead", type=int, default=2)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=16384)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-offload-compare", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the sharded path is "
+              "described, not built.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2503_10377_amd import sppo as L
+    from paper_2503_10377_amd.chunked import ChunkedAttention
+    from paper_2503_10377_amd.inputs import make_inputs
+
+    S, N, Hq, Hkv, D, offload = WORKLOADS[args.workload]
+    B = 1
+    torch.cuda.init()
+    inp = make_inputs(B, S, Hq, Hkv, D, torch.bfloat16, seed=0, device="cuda")
+    ca = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload=offload)
+    out = ca.alloc_outputs()
+    flops = algorithmic_flops(ca.offsets, B, Hq, D)
+
+    def timed(c, steps, timing):
+        for _ in range(args.warmup):
+            c.step(inp, out, lookahead=args.lookahead)
+        torch.cuda.synchronize()
+        L.sppo_copy_stats(c.ctx, reset_after=True)
+        L.sppo_set_kernel_timing(c.ctx, timing)
+        L.sppo_kernel_times(c.ctx, reset_after=True)
+        st = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(st)
+        for _ in range(steps):
+            c.step(inp, out, lookahead=args.lookahead)
+        e1.record(st)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        kt = L.sppo_kernel_times(c.ctx, reset_after=True)
+        cs = L.sppo_copy_stats(c.ctx, reset_after=True) if c.offload != L.SPPO_OFFLOAD_NONE else None
+        L.sppo_set_kernel_timing(c.ctx, False)
+        return ms, kt, cs
+
+    print(f"[bench] workload={args.workload} steps={args.steps} warmup={args.warmup}", file=sys.stderr, flush=True)
+    ms_on, kt, cs = timed(ca, args.steps, True)
+    print(f"[bench] ms/step={ms_on:.2f}", file=sys.stderr, flush=True)
+
+    res = {
+        "metric": METRIC, "value": None, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_on, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+    }
+    tflops = flops["total"] / (ms_on * 1e-3) / 1e12
+    res["value"] = tflops
+    res["pct_peak"] = 100.0 * tflops / PEAK_BF16_TFLOPS
+    res["tokens_per_s"] = S / (ms_on * 1e-3)
+    res["config"] = {
+        "workload": f"chunked causal attention fwd+bwd, batch {B}, seq {S} in {N} chunks of {S // N}, "
+                    f"{Hq} query / {Hkv} KV heads x head_dim {D}, bf16 in / fp32 accumulate, "
+                    f"offload {offload} (all chunks but the last), prefetch lookahead {args.lookahead}",
+        "name": args.workload, "batch": B, "seq_len": S, "n_chunks": N, "n_q_heads": Hq,
+        "n_kv_heads": Hkv, "head_dim": D, "offload": offload,
+    }
+    steps = args.steps
+    kern = {}
+    for name, v in kt.items():
+        per_step = v["ms"] / steps
+        k = {"ms_per_step": per_step, "launches_per_step": v["launches"] / steps}
+        if flops.get(name):
+            k["tflops"] = flops[name] / (per_step * 1e-3) / 1e12
+        kern[name] = k
+    res["kernels"] = kern
+    dom = max((n for n in kern if flops.get(n)), key=lambda n: kern[n]["ms_per_step"])
+    ach = kern[dom]["tflops"]
+    res["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
+                       "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": None}
+    if cs is not None:
+        copy_ms = (cs["ms_d2h"] + cs["ms_h2d"]) / steps
+        off = {"bytes_d2h_per_step": cs["bytes_d2h"] / steps, "bytes_h2d_per_step": cs["bytes_h2d"] / steps,
+               "copy_ms_per_step": copy_ms,
+               "d2h_GBps": cs["bytes_d2h"] / max(cs["ms_d2h"], 1e-9) / 1e6,
+               "h2d_GBps": cs["bytes_h2d"] / max(cs["ms_h2d"], 1e-9) / 1e6}
+        if not args.no_offload_compare:
+            ca_off = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="none")
+            ms_off, _, _ = timed(ca_off, steps, False)
+            ca_off.close()
+            exposed = max(0.0, ms_on - ms_off)
+            off["ms_per_step_no_offload"] = ms_off
+            off["exposed_ms_per_step"] = exposed
+            off["hidden_pct"] = 100.0 * max(0.0, min(1.0, 1.0 - exposed / copy_ms)) if copy_ms > 0 else None
+        res["offload"] = off
+        res["offload_hidden_pct"] = off.get("hidden_pct")
+    ca.close()
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cb = oracle_cpu_baseline(inp, D, args.cpu_sample_tokens)
+        res["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

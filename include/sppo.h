@@ -1,0 +1,218 @@
+/*
+ * libsppo -- sequence-chunked causal attention (forward + backward) with
+ * per-chunk activation offload to pinned host memory, for one MI355X (gfx950).
+ *
+ * The method is the single-GPU slice of Sequence Pipeline Parallel Offloading
+ * (SPPO, arXiv 2503.10377):
+ *   - The sequence of length S is split into N subsequences ("chunks") with
+ *     offsets c_0 = 0 < c_1 < ... < c_N = S (notation table: S, N, s_i).
+ *   - A query of chunk i attends to the keys/values of chunks 0..i
+ *     (Sec. 5.1, two-level activation management): every earlier chunk is
+ *     fully visible, the diagonal block carries the causal mask.  Keys and
+ *     values are the "skeletal" tensors and stay resident on the GPU.
+ *   - The other saved activations of chunk i (here Q_i, O_i, LSE_i, and
+ *     optionally a host copy of K_i/V_i) are offloaded to host memory while
+ *     the next chunk computes, and must be back on the device before the
+ *     backward of chunk i begins (Sec. 5.1, Sec. 5.2); page-locked host
+ *     buffers give the full host-link bandwidth (Sec. 7, implementation).
+ *   - The backward walks the chunks in reverse order and accumulates dK/dV.
+ *
+ * Layout (token-major BSHD, all tensors contiguous, device pointers unless
+ * stated otherwise, every pointer 16-byte aligned):
+ *   chunk-local  Q_i, O_i, dO_i, dQ_i : [B, s_i, Hq, D]   dtype of the problem
+ *   chunk-local  LSE_i                : [B, Hq, s_i]      fp32, natural log
+ *   full-length  K, V                 : [B, S, Hkv, D]    dtype of the problem
+ *   full-length  dK, dV accumulators  : [B, S, Hkv, D]    fp32
+ * Query head h reads KV head h / (Hq / Hkv).  With B = 1, chunk i of a full
+ * [1, S, H, D] tensor is the contiguous slab starting at row c_i.
+ *
+ * Threading and streams: a context is used from one host thread at a time.
+ * Every call is asynchronous with respect to the host on the stream it is
+ * given (a hipStream_t passed as void*; NULL is the legacy null stream),
+ * except sppo_copy_stats, sppo_sync and sppo_destroy, which block.  All
+ * backward calls of one context must be issued on one stream (they share the
+ * context's Delta workspace).
+ *
+ * Errors: every call returns an sppo_status.  Arguments are validated on the
+ * host before anything is enqueued; a failed call enqueues nothing.  A HIP
+ * error maps to SPPO_ERR_HIP; asynchronous device faults surface at the next
+ * call that synchronises.  sppo_last_error() holds a message for the last
+ * failure of that context.  Nothing aborts or throws across this ABI.
+ */
+#ifndef SPPO_H
+#define SPPO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sppo_ctx sppo_ctx;
+
+typedef enum {
+  SPPO_OK = 0,
+  SPPO_ERR_INVALID_ARG = 1, /* null/misaligned pointer, bad shape, bad index */
+  SPPO_ERR_UNSUPPORTED = 2, /* valid but not implemented (e.g. head_dim)     */
+  SPPO_ERR_ORDER = 3,       /* fwd not 0..N-1, or bwd not N-1..0           */
+  SPPO_ERR_STATE = 4,       /* e.g. prefetch of a chunk never offloaded    */
+  SPPO_ERR_OOM = 5,         /* device or pinned host allocation failed     */
+  SPPO_ERR_HIP = 6          /* a HIP runtime call failed                   */
+} sppo_status;
+
+typedef enum { SPPO_F32 = 0, SPPO_BF16 = 1 } sppo_dtype;
+
+/* Which saved activations of a chunk travel to host memory after its
+ * forward (two-level activation management, Sec. 5.1).  K/V always stay
+ * resident on the device as the skeletal level. */
+typedef enum {
+  SPPO_OFFLOAD_NONE = 0,  /* nothing leaves the device                      */
+  SPPO_OFFLOAD_QOL = 1,   /* Q_i, O_i, LSE_i offloaded and prefetched back  */
+  SPPO_OFFLOAD_QKVOL = 2  /* as QOL, plus a host copy of K_i and V_i; the
+                             resident K/V cache is not re-fetched           */
+} sppo_offload;
+
+/* The problem, in the paper's notation (B, S, N, s_i) plus the attention
+ * shape (query heads, KV heads, head dim).  Copied by sppo_create. */
+typedef struct {
+  int64_t batch;                 /* B >= 1                                  */
+  int64_t seq_len;               /* S >= 1                                  */
+  int32_t n_chunks;              /* N, 1 <= N <= S                          */
+  const int64_t* chunk_offsets;  /* host array of N+1 offsets, strictly
+                                    increasing from 0 to S; NULL means N
+                                    equal chunks (requires S % N == 0)      */
+  int32_t n_q_heads;             /* Hq >= 1                                 */
+  int32_t n_kv_heads;            /* Hkv >= 1, Hq % Hkv == 0                 */
+  int32_t head_dim;              /* D in {64, 128}                          */
+  sppo_dtype dtype;              /* element type of Q, K, V, O, dO, dQ      */
+  float softmax_scale;           /* 0 means 1/sqrt(D)                       */
+  sppo_offload offload;          /* offload set; NONE allocates no host mem */
+} sppo_problem;
+
+/* Device pointers of one chunk's saved activations, for offload/prefetch. */
+typedef struct {
+  void* q;      /* Q_i   [B, s_i, Hq, D]  chunk-local                        */
+  void* o;      /* O_i   [B, s_i, Hq, D]  chunk-local                        */
+  float* lse;   /* LSE_i [B, Hq, s_i]     chunk-local                        */
+  void* k;      /* base of the full K cache [B, S, Hkv, D]; rows of chunk i  */
+  void* v;      /* base of the full V cache [B, S, Hkv, D]; rows of chunk i  */
+} sppo_chunk_bufs;
+
+typedef struct {
+  uint64_t bytes_d2h;    /* bytes copied device->host since create/reset  */
+  uint64_t bytes_h2d;    /* bytes copied host->device                     */
+  double ms_d2h;         /* sum over chunks of event-timed D2H durations   */
+  double ms_h2d;         /* sum over chunks of event-timed H2D durations   */
+  int32_t n_d2h;         /* chunks offloaded                               */
+  int32_t n_h2d;         /* chunks prefetched                              */
+} sppo_copy_stats_t;
+
+/* Kernels of one chunk, for per-kernel timing. */
+typedef enum {
+  SPPO_KERNEL_FWD = 0,       /* forward of a chunk                          */
+  SPPO_KERNEL_BWD_PRE = 1,   /* Delta = rowsum(dO * O)                      */
+  SPPO_KERNEL_BWD_DKDV = 2,  /* dK/dV accumulation over the chunk's queries */
+  SPPO_KERNEL_BWD_DQ = 3,    /* dQ of the chunk                             */
+  SPPO_KERNEL_COUNT = 4
+} sppo_kernel;
+
+typedef struct {
+  double ms[SPPO_KERNEL_COUNT];         /* summed event-timed durations     */
+  int32_t launches[SPPO_KERNEL_COUNT];  /* launches timed                   */
+} sppo_kernel_times_t;
+
+/* Create a context: validates the problem, copies the offsets, allocates
+ * the Delta workspace (fp32 [B, Hq, max s_i]) on the current device, two
+ * copy streams (default priority) and per-chunk events, and -- unless
+ * offload is NONE -- page-locked host slots for every chunk's offload set.
+ * *out is set only on success.  Errors: INVALID_ARG, UNSUPPORTED, OOM, HIP. */
+sppo_status sppo_create(const sppo_problem* problem, sppo_ctx** out);
+
+/* Synchronise the context's copy streams and free everything it owns.
+ * Safe on NULL. */
+sppo_status sppo_destroy(sppo_ctx* ctx);
+
+/* Forward of chunk i (Sec. 5.1): for rows r in [c_i, c_{i+1}) and every
+ * query head, O_i[r] = softmax over keys j <= r (global positions) of
+ * scale * Q_i[r].K[j], applied to V; LSE_i[r] = log sum_j exp(scale*Q.K).
+ * Reads K/V rows [0, c_{i+1}).  Calls must come in order i = 0..N-1 (the
+ * first call after create, after sppo_reset, or after bwd(0) must be
+ * i = 0); otherwise ORDER and nothing is enqueued. */
+sppo_status sppo_attn_fwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i,
+                                const void* k, const void* v, void* o_i,
+                                float* lse_i, void* stream);
+
+/* Backward of chunk i in the reverse walk (Sec. 5.2): with Delta_r =
+ * <dO_r, O_r>, P = exp(scale*Q.K - LSE), dS = P (dO.V - Delta):
+ *   dQ_i = scale * dS K                         (written)
+ *   dK[0, c_{i+1}) += scale * dS^T Q_i,  dV[0, c_{i+1}) += P^T dO_i
+ * For i = N-1 (the first backward call) dK/dV rows [0, S) are overwritten,
+ * so the accumulators need no zeroing; rows >= c_{i+1} are never touched.
+ * Calls must come in order i = N-1..0 after fwd(N-1).  If chunk i was
+ * offloaded, the stream first waits for the prefetch of chunk i, which must
+ * have been issued (otherwise STATE). */
+sppo_status sppo_attn_bwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i,
+                                const void* k, const void* v, const void* o_i,
+                                const float* lse_i, const void* do_i,
+                                void* dq_i, float* dk_acc, float* dv_acc,
+                                void* stream);
+
+/* Offload chunk i's saved activations (the set chosen by problem.offload)
+ * from the device pointers in *src to the context's pinned host slot i.
+ * Records an event on `stream` (after the fwd of chunk i); the context's
+ * D2H stream waits for it, copies, and records the chunk's offload-done
+ * event.  The device sources must not be overwritten until that event --
+ * see sppo_offload_wait.  Requires fwd(i) issued, offload != NONE. */
+sppo_status sppo_offload_issue(sppo_ctx* ctx, int32_t i,
+                               const sppo_chunk_bufs* src, void* stream);
+
+/* Make `stream` wait until chunk i's offload copies have completed (its
+ * device buffers may then be reused or overwritten).  Requires the offload
+ * of chunk i to have been issued. */
+sppo_status sppo_offload_wait(sppo_ctx* ctx, int32_t i, void* stream);
+
+/* Prefetch chunk i's offloaded Q/O/LSE from host slot i into the device
+ * pointers in *dst (K/V are never re-fetched: the cache is resident).  The
+ * H2D stream waits for an event recorded now on `stream` (so dst may be
+ * written after everything already enqueued there) and for chunk i's
+ * offload-done event; the backward of chunk i then waits for the copy.
+ * Requires the offload of chunk i to have been issued. */
+sppo_status sppo_prefetch(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* dst,
+                          void* stream);
+
+/* Abandon the current forward/backward walk (e.g. after a forward-only run):
+ * the next call must be fwd(0).  Clears per-chunk offload state. */
+sppo_status sppo_reset(sppo_ctx* ctx);
+
+/* Block until the context's copy streams are idle. */
+sppo_status sppo_sync(sppo_ctx* ctx);
+
+/* Synchronise the copy streams and return cumulative copy statistics;
+ * `reset_after` != 0 zeroes them afterwards. */
+sppo_status sppo_copy_stats(sppo_ctx* ctx, sppo_copy_stats_t* out, int32_t reset_after);
+
+/* Enable (1) or disable (0) per-kernel timing: while enabled, every kernel
+ * launch is bracketed by two events on the caller's stream.  Creates the
+ * events on first use. */
+sppo_status sppo_set_kernel_timing(sppo_ctx* ctx, int32_t enable);
+
+/* Wait for the timed kernels and return the summed durations and launch
+ * counts per kernel since the last reset; `reset_after` != 0 zeroes them. */
+sppo_status sppo_kernel_times(sppo_ctx* ctx, sppo_kernel_times_t* out, int32_t reset_after);
+
+/* Chunk offsets as stored by the context (n_chunks + 1 values). */
+sppo_status sppo_get_offsets(const sppo_ctx* ctx, int64_t* out, int32_t capacity);
+
+/* Message for the last failure of this context ("" if none); with
+ * ctx == NULL, the message of the last failed sppo_create on this thread. */
+const char* sppo_last_error(const sppo_ctx* ctx);
+
+/* Static name of a status code. */
+const char* sppo_status_string(sppo_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPPO_H */

@@ -1,0 +1,9 @@
+"""libsppo: sequence-chunked causal attention (forward + backward) with
+per-chunk activation offload, for MI355X (gfx950).
+
+``sppo``     ctypes binding of the C ABI in include/sppo.h
+``chunked``  the chunk loop (forward walk with offload, reverse backward
+             walk with prefetch) over that ABI
+``inputs``   seeded synthetic inputs
+``build``    in-tree hipcc build of libsppo.so
+"""

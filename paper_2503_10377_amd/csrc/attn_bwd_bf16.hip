@@ -1,0 +1,393 @@
+// Backward of one chunk of sequence-chunked causal attention, bf16 in / fp32
+// accumulate, for gfx950 (MI355X).  The reverse walk over chunks (Sec. 5.2
+// of SPPO) calls this for i = N-1..0; dK/dV accumulate across calls in fp32.
+//
+// Three kernels, all on the caller's stream:
+//   bwd_pre   Delta_r = <dO_r, O_r>                      (HBM-bound)
+//   bwd_dkdv  one workgroup per 128 keys of one KV head (4 waves x 32 keys,
+//             lane <-> key); streams the chunk's query tiles (64 rows, every
+//             query head of the GQA group) through LDS and accumulates
+//               dV += P^T dO,  dK += scale * dS^T Q
+//             in registers; S = Q K^T and dP = dO V^T are recomputed.
+//   bwd_dq    one workgroup per 128 query rows of one head (lane <-> query);
+//             streams K/V tiles and accumulates dQ^T += K^T dS^T.
+// P = exp2(S*scale*log2e - LSE*log2e), dS = P (dP - Delta).
+#include "sppo_kernels.h"
+#include "tile_common.h"
+
+namespace sppo {
+namespace {
+
+constexpr int kDqBR = 128;    // query rows per dq workgroup
+constexpr int kDqBC = 64;     // keys per dq K/V tile
+constexpr int kKvBKV = 128;   // keys per dkdv workgroup
+constexpr int kKvBQ = 64;     // query rows per dkdv query tile
+
+// ------------------------------------------------------------------ Delta
+template <int D>
+__global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(ChunkArgs a) {
+  constexpr int LPI = D / 8;  // lanes per (b, r, h) row, 8 bf16 each
+  const int64_t s = a.c1 - a.c0;
+  const int64_t nrows = a.B * s * a.Hq;
+  const int64_t item = ((int64_t)blockIdx.x * 256 + threadIdx.x) / LPI;
+  const int sub = threadIdx.x % LPI;
+  float acc = 0.f;
+  if (item < nrows) {
+    const u32x4 ov = ld_global16(static_cast<const uint16_t*>(a.o) + item * D + 8 * sub);
+    const u32x4 dv = ld_global16(static_cast<const uint16_t*>(a.dout) + item * D + 8 * sub);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc += __uint_as_float(ov[e] << 16) * __uint_as_float(dv[e] << 16);
+      acc += __uint_as_float(ov[e] & 0xffff0000u) * __uint_as_float(dv[e] & 0xffff0000u);
+    }
+  }
+#pragma unroll
+  for (int off = LPI / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (item < nrows && sub == 0) {
+    const int64_t h = item % a.Hq;
+    const int64_t rr = (item / a.Hq) % s;
+    const int64_t b = item / (a.Hq * s);
+    a.delta[(b * a.Hq + h) * s + rr] = acc;
+  }
+}
+
+// --------------------------------------------------------------------- dQ
+template <int D>
+__global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
+  constexpr int BR = kDqBR, BC = kDqBC;
+  constexpr int KP = D + 8, TP = BC + 4;
+  constexpr int NK = D / 16, ND = D / 32, CG = D / 8;
+  constexpr int ITEMS = (BC / 4) * CG;
+  constexpr int IPT = (ITEMS + 255) / 256;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[BC * KP];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[BC * KP];
+  __shared__ __attribute__((aligned(16))) uint16_t Kt[D * TP];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l32 = lane & 31, g = lane >> 5;
+  const int t = gridDim.x - 1 - blockIdx.x;
+  const int h = blockIdx.y;
+  const int64_t b = blockIdx.z;
+  const int hk = h / (a.Hq / a.Hkv);
+  const int64_t c0 = a.c0, c1 = a.c1, s = c1 - c0;
+  const int64_t q0 = c0 + (int64_t)t * BR;
+  const int64_t r = q0 + w * 32 + l32;
+  const bool rvalid = r < c1;
+  const int64_t kend = (q0 + BR < c1) ? q0 + BR : c1;
+  const int nkv = (int)((kend + BC - 1) / BC);
+  const float C = a.scale * kLog2e;
+
+  bf16x8 qf[NK], df[NK];
+  float lse2 = INFINITY, dl = 0.f;
+  if (rvalid) {
+    const int64_t off = ((b * s + (r - c0)) * a.Hq + h) * D;
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + off;
+    const uint16_t* drow = static_cast<const uint16_t*>(a.dout) + off;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      qf[kk] = as_bf16x8(ld_global16(qrow + 16 * kk + 8 * g));
+      df[kk] = as_bf16x8(ld_global16(drow + 16 * kk + 8 * g));
+    }
+    lse2 = a.lse[(b * a.Hq + h) * s + (r - c0)] * kLog2e;
+    dl = a.delta[(b * a.Hq + h) * s + (r - c0)];
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) qf[kk] = df[kk] = bf16x8{};
+  }
+
+  const int64_t kvstride = (int64_t)a.Hkv * D;
+  const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + (b * a.S * a.Hkv + hk) * D;
+  const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + (b * a.S * a.Hkv + hk) * D;
+
+  f32x16 dq[ND];
+#pragma unroll
+  for (int db = 0; db < ND; ++db) dq[db] = f32x16{};
+
+  Block4x8 kreg[IPT], vreg[IPT];
+  auto load_tile = [&](int it) {
+    const int64_t k0 = (int64_t)it * BC;
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+      const int c = tid + 256 * u;
+      if (ITEMS % 256 == 0 || c < ITEMS) {
+        const int rg = c / CG, cg = c % CG;
+        load_block4x8(kreg[u], kbase, kvstride, k0 + 4 * rg, c1, 8 * cg);
+        load_block4x8(vreg[u], vbase, kvstride, k0 + 4 * rg, c1, 8 * cg);
+      }
+    }
+  };
+
+  load_tile(0);
+  for (int it = 0; it < nkv; ++it) {
+    const int64_t k0 = (int64_t)it * BC;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+      const int c = tid + 256 * u;
+      if (ITEMS % 256 == 0 || c < ITEMS) {
+        const int rg = c / CG, cg = c % CG;
+        store_block_nat(kreg[u], Ks, KP, 4 * rg, 8 * cg);
+        store_block_trans(kreg[u], Kt, TP, 4 * rg, 8 * cg);
+        store_block_nat(vreg[u], Vs, KP, 4 * rg, 8 * cg);
+      }
+    }
+    __syncthreads();
+    if (it + 1 < nkv) load_tile(it + 1);
+
+    const bool need_mask = k0 + BC - 1 > q0 + 32 * w;
+    bf16x8 dsb[4];
+#pragma unroll
+    for (int jb = 0; jb < 2; ++jb) {
+      f32x16 sv = f32x16{}, dp = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        sv = mfma32(ld_lds16(Ks + (32 * jb + l32) * KP + 16 * kk + 8 * g), qf[kk], sv);
+        dp = mfma32(ld_lds16(Vs + (32 * jb + l32) * KP + 16 * kk + 8 * g), df[kk], dp);
+      }
+      float ds[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float p = fast_exp2(sv[v] * C - lse2);
+        if (need_mask) {
+          const int64_t key = k0 + 32 * jb + 8 * (v / 4) + 4 * g + (v % 4);
+          if (key > r) p = 0.f;
+        }
+        ds[v] = p * (dp[v] - dl);
+      }
+      dsb[2 * jb] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
+      dsb[2 * jb + 1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
+    }
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+#pragma unroll
+      for (int kb = 0; kb < BC / 16; ++kb) {
+        dq[db] = mfma32(ld_lds_perm(Kt + (32 * db + l32) * TP + 16 * kb + 4 * g), dsb[kb], dq[db]);
+      }
+    }
+  }
+
+  if (rvalid) {
+    uint16_t* qrow = static_cast<uint16_t*>(a.dq) + ((b * s + (r - c0)) * a.Hq + h) * D;
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        bf16x2 lo, hi;
+        lo.x = (__bf16)(dq[db][4 * q4 + 0] * a.scale);
+        lo.y = (__bf16)(dq[db][4 * q4 + 1] * a.scale);
+        hi.x = (__bf16)(dq[db][4 * q4 + 2] * a.scale);
+        hi.y = (__bf16)(dq[db][4 * q4 + 3] * a.scale);
+        u32x2 wv = {__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+        *reinterpret_cast<u32x2*>(qrow + 32 * db + 8 * q4 + 4 * g) = wv;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ dK dV
+template <int D>
+__global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
+  constexpr int BQ = kKvBQ;
+  constexpr int KP = D + 8, TQ = BQ + 4;
+  constexpr int NK = D / 16, ND = D / 32, CG = D / 8;
+  constexpr int ITEMS = (BQ / 4) * CG;
+  constexpr int IPT = (ITEMS + 255) / 256;
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[BQ * KP];
+  __shared__ __attribute__((aligned(16))) uint16_t Ds[BQ * KP];
+  __shared__ __attribute__((aligned(16))) uint16_t Qt[D * TQ];
+  __shared__ __attribute__((aligned(16))) uint16_t Dt[D * TQ];
+  __shared__ __attribute__((aligned(16))) float lse2s[BQ];
+  __shared__ __attribute__((aligned(16))) float dls[BQ];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l32 = lane & 31, g = lane >> 5;
+  const int hk = blockIdx.y;
+  const int64_t b = blockIdx.z;
+  const int G = a.Hq / a.Hkv;
+  const int64_t c0 = a.c0, c1 = a.c1, s = c1 - c0;
+  const int64_t k0 = (int64_t)blockIdx.x * kKvBKV;
+  const int64_t j = k0 + 32 * w + l32;  // this lane's key
+  const float C = a.scale * kLog2e;
+
+  bf16x8 kf[NK], vf[NK];
+  {
+    const int64_t off = ((b * a.S + j) * a.Hkv + hk) * D;
+    const uint16_t* krow = static_cast<const uint16_t*>(a.k) + off;
+    const uint16_t* vrow = static_cast<const uint16_t*>(a.v) + off;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      kf[kk] = j < c1 ? as_bf16x8(ld_global16(krow + 16 * kk + 8 * g)) : bf16x8{};
+      vf[kk] = j < c1 ? as_bf16x8(ld_global16(vrow + 16 * kk + 8 * g)) : bf16x8{};
+    }
+  }
+
+  f32x16 dk[ND], dv[ND];
+#pragma unroll
+  for (int db = 0; db < ND; ++db) dk[db] = dv[db] = f32x16{};
+
+  // Query tiles (chunk-local) that can see a key of this workgroup.
+  const int64_t qt_begin = k0 > c0 ? (k0 - c0) / BQ : 0;
+  const int64_t nqt = (s + BQ - 1) / BQ;
+  const int64_t per_head = nqt - qt_begin;
+  const int64_t total = per_head * G;
+
+  const int64_t qstride = (int64_t)a.Hq * D;
+  Block4x8 qreg[IPT], dreg[IPT];
+  float lse_r = INFINITY, dl_r = 0.f;
+  auto load_tile = [&](int64_t n) {
+    const int h = hk * G + (int)(n / per_head);
+    const int64_t qt = qt_begin + n % per_head;
+    const uint16_t* qbase = static_cast<const uint16_t*>(a.q) + (b * s * a.Hq + h) * D;
+    const uint16_t* dbase = static_cast<const uint16_t*>(a.dout) + (b * s * a.Hq + h) * D;
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+      const int c = tid + 256 * u;
+      if (ITEMS % 256 == 0 || c < ITEMS) {
+        const int rg = c / CG, cg = c % CG;
+        load_block4x8(qreg[u], qbase, qstride, qt * BQ + 4 * rg, s, 8 * cg);
+        load_block4x8(dreg[u], dbase, qstride, qt * BQ + 4 * rg, s, 8 * cg);
+      }
+    }
+    if (tid < BQ) {
+      const int64_t rr = qt * BQ + tid;
+      if (rr < s) {
+        lse_r = a.lse[(b * a.Hq + h) * s + rr] * kLog2e;
+        dl_r = a.delta[(b * a.Hq + h) * s + rr];
+      } else {
+        lse_r = INFINITY;
+        dl_r = 0.f;
+      }
+    }
+  };
+
+  if (total > 0) load_tile(0);
+  for (int64_t n = 0; n < total; ++n) {
+    const int64_t q0 = c0 + (qt_begin + n % per_head) * BQ;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+      const int c = tid + 256 * u;
+      if (ITEMS % 256 == 0 || c < ITEMS) {
+        const int rg = c / CG, cg = c % CG;
+        store_block_nat(qreg[u], Qs, KP, 4 * rg, 8 * cg);
+        store_block_trans(qreg[u], Qt, TQ, 4 * rg, 8 * cg);
+        store_block_nat(dreg[u], Ds, KP, 4 * rg, 8 * cg);
+        store_block_trans(dreg[u], Dt, TQ, 4 * rg, 8 * cg);
+      }
+    }
+    if (tid < BQ) {
+      lse2s[tid] = lse_r;
+      dls[tid] = dl_r;
+    }
+    __syncthreads();
+    if (n + 1 < total) load_tile(n + 1);
+
+#pragma unroll
+    for (int ib = 0; ib < BQ / 32; ++ib) {
+      // S[query][key] = Q K^T and dP = dO V^T; lane <-> key.
+      f32x16 sv = f32x16{}, dp = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        sv = mfma32(ld_lds16(Qs + (32 * ib + l32) * KP + 16 * kk + 8 * g), kf[kk], sv);
+        dp = mfma32(ld_lds16(Ds + (32 * ib + l32) * KP + 16 * kk + 8 * g), vf[kk], dp);
+      }
+      const bool need_mask = k0 + 32 * w + 31 > q0 + 32 * ib;
+      float p[16], ds[16];
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const int qi = 32 * ib + 8 * v4 + 4 * g;
+        const float4 l4 = *reinterpret_cast<const float4*>(lse2s + qi);
+        const float4 d4 = *reinterpret_cast<const float4*>(dls + qi);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int v = 4 * v4 + e;
+          float pv = fast_exp2(sv[v] * C - lv[e]);
+          if (need_mask && j > q0 + qi + e) pv = 0.f;
+          p[v] = pv;
+          ds[v] = pv * (dp[v] - dv4[e]);
+        }
+      }
+      bf16x8 pb[2], dsb[2];
+      pb[0] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+      pb[1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
+      dsb[0] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
+      dsb[1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
+      // dV[key][d] += P^T dO,  dK[key][d] += dS^T Q   (lane <-> d in C).
+#pragma unroll
+      for (int db = 0; db < ND; ++db) {
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int kb = 2 * ib + hh;
+          dv[db] = mfma32(pb[hh], ld_lds_perm(Dt + (32 * db + l32) * TQ + 16 * kb + 4 * g), dv[db]);
+          dk[db] = mfma32(dsb[hh], ld_lds_perm(Qt + (32 * db + l32) * TQ + 16 * kb + 4 * g), dk[db]);
+        }
+      }
+    }
+  }
+
+  // Write back rows [k0, k0+128) n [0, c1): lane <-> d, v <-> key.
+#pragma unroll
+  for (int db = 0; db < ND; ++db) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t key = k0 + 32 * w + 8 * (v / 4) + 4 * g + (v % 4);
+      if (key < c1) {
+        const int64_t idx = ((b * a.S + key) * a.Hkv + hk) * D + 32 * db + l32;
+        const float kval = dk[db][v] * a.scale;
+        const float vval = dv[db][v];
+        if (a.accumulate) {
+          a.dk[idx] += kval;
+          a.dv[idx] += vval;
+        } else {
+          a.dk[idx] = kval;
+          a.dv[idx] = vval;
+        }
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_bwd_pre_bf16(const ChunkArgs& a, hipStream_t stream) {
+  const int64_t s = a.c1 - a.c0;
+  const int64_t threads = a.B * s * a.Hq * (a.D / 8);
+  dim3 grid((unsigned)((threads + 255) / 256));
+  if (a.D == 128) {
+    hipLaunchKernelGGL(bwd_pre_bf16_kernel<128>, grid, dim3(256), 0, stream, a);
+  } else if (a.D == 64) {
+    hipLaunchKernelGGL(bwd_pre_bf16_kernel<64>, grid, dim3(256), 0, stream, a);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dkdv_bf16(const ChunkArgs& a, hipStream_t stream) {
+  dim3 grid((unsigned)((a.c1 + kKvBKV - 1) / kKvBKV), (unsigned)a.Hkv, (unsigned)a.B);
+  if (a.D == 128) {
+    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, grid, dim3(256), 0, stream, a);
+  } else if (a.D == 64) {
+    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<64>, grid, dim3(256), 0, stream, a);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq_bf16(const ChunkArgs& a, hipStream_t stream) {
+  const int64_t s = a.c1 - a.c0;
+  dim3 grid((unsigned)((s + kDqBR - 1) / kDqBR), (unsigned)a.Hq, (unsigned)a.B);
+  if (a.D == 128) {
+    hipLaunchKernelGGL(bwd_dq_bf16_kernel<128>, grid, dim3(256), 0, stream, a);
+  } else if (a.D == 64) {
+    hipLaunchKernelGGL(bwd_dq_bf16_kernel<64>, grid, dim3(256), 0, stream, a);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sppo

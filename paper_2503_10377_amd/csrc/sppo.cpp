@@ -1,0 +1,584 @@
+// libsppo host side: the C ABI declared in include/sppo.h.
+//
+// Owns, per context: the chunk partition (offsets c_0..c_N), a Delta
+// workspace on the device, two non-blocking copy streams (device->host and
+// host->device, default priority), per-chunk events, and page-locked host
+// slots holding each chunk's offload set.  Kernels run on the caller's
+// stream; copies run on the context's streams and are ordered against the
+// caller's stream with events only, so nothing blocks the host.
+//
+// Offload protocol for chunk i (two-level activation management, Sec. 5.1;
+// sequence-aware offloading overlaps chunk i's copy with chunk i+1's
+// compute, Sec. 5.2):
+//   offload_issue(i): record E_fwd[i] on the caller stream; the D2H stream
+//                     waits for it, copies the offload set to host slot i
+//                     and records E_off[i].
+//   prefetch(i)     : record E_call[i] on the caller stream; the H2D stream
+//                     waits for E_call[i] and E_off[i], copies Q/O/LSE back
+//                     and records E_pf[i].
+//   bwd_chunk(i)    : the caller stream waits for E_pf[i] before its kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "sppo.h"
+#include "sppo_kernels.h"
+
+namespace {
+
+struct EventPair {
+  hipEvent_t start = nullptr, stop = nullptr;
+  bool pending = false;  // recorded and not yet folded into the totals
+};
+
+struct HostSlot {
+  void* base = nullptr;  // one pinned allocation per chunk
+  void* q = nullptr;
+  void* o = nullptr;
+  void* lse = nullptr;
+  void* k = nullptr;
+  void* v = nullptr;
+};
+
+}  // namespace
+
+struct sppo_ctx {
+  sppo_problem prob{};
+  std::vector<int64_t> off;
+  int64_t s_max = 0;
+  size_t elt = 0;
+  float scale = 0.f;
+  int device = 0;
+  hipStream_t d2h = nullptr, h2d = nullptr;
+  float* delta = nullptr;
+  std::vector<HostSlot> slots;
+  std::vector<hipEvent_t> ev_fwd, ev_off, ev_call, ev_pf;
+  std::vector<EventPair> t_d2h, t_h2d;
+  std::vector<uint8_t> offloaded, prefetched;
+  bool in_bwd = false;
+  int next_fwd = 0, next_bwd = -1;
+  uint64_t bytes_d2h = 0, bytes_h2d = 0;
+  double ms_d2h = 0.0, ms_h2d = 0.0;
+  int32_t n_d2h = 0, n_h2d = 0;
+  bool ktiming = false;
+  std::vector<EventPair> t_kern[SPPO_KERNEL_COUNT];
+  double kms[SPPO_KERNEL_COUNT] = {};
+  int32_t klaunch[SPPO_KERNEL_COUNT] = {};
+  std::string err;
+};
+
+namespace {
+
+thread_local std::string g_create_error;
+
+sppo_status fail(sppo_ctx* ctx, sppo_status st, const std::string& msg) {
+  if (ctx) {
+    ctx->err = msg;
+  } else {
+    g_create_error = msg;
+  }
+  return st;
+}
+
+sppo_status hip_fail(sppo_ctx* ctx, hipError_t e, const char* what) {
+  return fail(ctx, SPPO_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define SPPO_HIP(ctx, call)                                  \
+  do {                                                       \
+    hipError_t e_ = (call);                                  \
+    if (e_ != hipSuccess) return hip_fail((ctx), e_, #call); \
+  } while (0)
+
+bool aligned16(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int64_t chunk_len(const sppo_ctx* c, int i) { return c->off[i + 1] - c->off[i]; }
+
+size_t bytes_q(const sppo_ctx* c, int i) {  // also O
+  return (size_t)c->prob.batch * chunk_len(c, i) * c->prob.n_q_heads * c->prob.head_dim * c->elt;
+}
+size_t bytes_lse(const sppo_ctx* c, int i) {
+  return (size_t)c->prob.batch * c->prob.n_q_heads * chunk_len(c, i) * sizeof(float);
+}
+size_t bytes_kv_row_block(const sppo_ctx* c, int i) {  // one batch entry's K_i rows
+  return (size_t)chunk_len(c, i) * c->prob.n_kv_heads * c->prob.head_dim * c->elt;
+}
+bool offload_kv(const sppo_ctx* c) { return c->prob.offload == SPPO_OFFLOAD_QKVOL; }
+
+sppo_status check_ctx_index(sppo_ctx* ctx, int32_t i) {
+  if (!ctx) return SPPO_ERR_INVALID_ARG;
+  if (i < 0 || i >= ctx->prob.n_chunks) {
+    return fail(ctx, SPPO_ERR_INVALID_ARG, "chunk index " + std::to_string(i) + " out of range");
+  }
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != ctx->device) {
+    return fail(ctx, SPPO_ERR_STATE, "the context's device is not the current device");
+  }
+  return SPPO_OK;
+}
+
+sppo_status check_ptr(sppo_ctx* ctx, const void* p, const char* name) {
+  if (!aligned16(p)) {
+    return fail(ctx, SPPO_ERR_INVALID_ARG, std::string(name) + " is null or not 16-byte aligned");
+  }
+  return SPPO_OK;
+}
+
+sppo::ChunkArgs make_args(const sppo_ctx* c, int i) {
+  sppo::ChunkArgs a{};
+  a.B = c->prob.batch;
+  a.S = c->prob.seq_len;
+  a.c0 = c->off[i];
+  a.c1 = c->off[i + 1];
+  a.Hq = c->prob.n_q_heads;
+  a.Hkv = c->prob.n_kv_heads;
+  a.D = c->prob.head_dim;
+  a.scale = c->scale;
+  a.delta = c->delta;
+  return a;
+}
+
+// Fold a finished timing pair into the totals (waits for it if needed).
+void fold(EventPair& p, double& total) {
+  if (!p.pending) return;
+  float ms = 0.f;
+  if (hipEventSynchronize(p.stop) == hipSuccess && hipEventElapsedTime(&ms, p.start, p.stop) == hipSuccess) {
+    total += ms;
+  }
+  p.pending = false;
+}
+
+// Launch one kernel, bracketed by timing events when kernel timing is on.
+template <class F>
+hipError_t timed_launch(sppo_ctx* c, int kind, int i, hipStream_t s, F&& launch) {
+  if (!c->ktiming) return launch();
+  EventPair& p = c->t_kern[kind][i];
+  fold(p, c->kms[kind]);
+  hipError_t e = hipEventRecord(p.start, s);
+  if (e != hipSuccess) return e;
+  if ((e = launch()) != hipSuccess) return e;
+  if ((e = hipEventRecord(p.stop, s)) != hipSuccess) return e;
+  p.pending = true;
+  c->klaunch[kind] += 1;
+  return hipSuccess;
+}
+
+void destroy_all(sppo_ctx* c) {
+  if (c->d2h) (void)hipStreamSynchronize(c->d2h);
+  if (c->h2d) (void)hipStreamSynchronize(c->h2d);
+  for (auto* v : {&c->ev_fwd, &c->ev_off, &c->ev_call, &c->ev_pf}) {
+    for (hipEvent_t e : *v) {
+      if (e) (void)hipEventDestroy(e);
+    }
+  }
+  for (auto* v : {&c->t_d2h, &c->t_h2d, &c->t_kern[0], &c->t_kern[1], &c->t_kern[2], &c->t_kern[3]}) {
+    for (EventPair& p : *v) {
+      if (p.start) (void)hipEventDestroy(p.start);
+      if (p.stop) (void)hipEventDestroy(p.stop);
+    }
+  }
+  for (HostSlot& s : c->slots) {
+    if (s.base) (void)hipHostFree(s.base);
+  }
+  if (c->delta) (void)hipFree(c->delta);
+  if (c->d2h) (void)hipStreamDestroy(c->d2h);
+  if (c->h2d) (void)hipStreamDestroy(c->h2d);
+  delete c;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sppo_status_string(sppo_status s) {
+  switch (s) {
+    case SPPO_OK: return "SPPO_OK";
+    case SPPO_ERR_INVALID_ARG: return "SPPO_ERR_INVALID_ARG";
+    case SPPO_ERR_UNSUPPORTED: return "SPPO_ERR_UNSUPPORTED";
+    case SPPO_ERR_ORDER: return "SPPO_ERR_ORDER";
+    case SPPO_ERR_STATE: return "SPPO_ERR_STATE";
+    case SPPO_ERR_OOM: return "SPPO_ERR_OOM";
+    case SPPO_ERR_HIP: return "SPPO_ERR_HIP";
+  }
+  return "SPPO_ERR_UNKNOWN";
+}
+
+const char* sppo_last_error(const sppo_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_create_error.c_str();
+}
+
+sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
+  g_create_error.clear();
+  if (!p || !out) return fail(nullptr, SPPO_ERR_INVALID_ARG, "null problem or output pointer");
+  if (p->batch < 1 || p->seq_len < 1 || p->n_chunks < 1 || p->n_chunks > p->seq_len) {
+    return fail(nullptr, SPPO_ERR_INVALID_ARG, "need batch >= 1, seq_len >= 1, 1 <= n_chunks <= seq_len");
+  }
+  if (p->n_q_heads < 1 || p->n_kv_heads < 1 || p->n_q_heads % p->n_kv_heads != 0) {
+    return fail(nullptr, SPPO_ERR_INVALID_ARG, "need n_q_heads a positive multiple of n_kv_heads");
+  }
+  if (p->n_q_heads > 65535 || p->n_kv_heads > 65535 || p->batch > 65535) {
+    return fail(nullptr, SPPO_ERR_UNSUPPORTED, "batch and head counts above 65535 are not supported");
+  }
+  if (p->dtype != SPPO_F32 && p->dtype != SPPO_BF16) {
+    return fail(nullptr, SPPO_ERR_INVALID_ARG, "unknown dtype");
+  }
+  if (p->head_dim != 64 && p->head_dim != 128) {
+    return fail(nullptr, SPPO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  }
+  if (p->offload != SPPO_OFFLOAD_NONE && p->offload != SPPO_OFFLOAD_QOL && p->offload != SPPO_OFFLOAD_QKVOL) {
+    return fail(nullptr, SPPO_ERR_INVALID_ARG, "unknown offload mode");
+  }
+  if (!(p->softmax_scale >= 0.f) || std::isinf(p->softmax_scale)) {
+    return fail(nullptr, SPPO_ERR_INVALID_ARG, "softmax_scale must be finite and >= 0 (0 = 1/sqrt(D))");
+  }
+  std::vector<int64_t> off(p->n_chunks + 1);
+  if (p->chunk_offsets) {
+    for (int i = 0; i <= p->n_chunks; ++i) off[i] = p->chunk_offsets[i];
+    if (off[0] != 0 || off[p->n_chunks] != p->seq_len) {
+      return fail(nullptr, SPPO_ERR_INVALID_ARG, "chunk_offsets must start at 0 and end at seq_len");
+    }
+    for (int i = 0; i < p->n_chunks; ++i) {
+      if (off[i + 1] <= off[i]) return fail(nullptr, SPPO_ERR_INVALID_ARG, "chunk_offsets must increase strictly");
+    }
+  } else {
+    if (p->seq_len % p->n_chunks != 0) {
+      return fail(nullptr, SPPO_ERR_INVALID_ARG, "equal chunks need seq_len % n_chunks == 0");
+    }
+    for (int i = 0; i <= p->n_chunks; ++i) off[i] = (p->seq_len / p->n_chunks) * i;
+  }
+
+  sppo_ctx* c = new (std::nothrow) sppo_ctx();
+  if (!c) return fail(nullptr, SPPO_ERR_OOM, "host allocation of the context failed");
+  c->prob = *p;
+  c->prob.chunk_offsets = nullptr;
+  c->off = std::move(off);
+  c->elt = p->dtype == SPPO_BF16 ? 2 : 4;
+  c->scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / std::sqrt((float)p->head_dim);
+  for (int i = 0; i < p->n_chunks; ++i) c->s_max = std::max<int64_t>(c->s_max, chunk_len(c, i));
+
+  auto bail = [&](sppo_status st, const std::string& msg) {
+    destroy_all(c);
+    return fail(nullptr, st, msg);
+  };
+  hipError_t e = hipGetDevice(&c->device);
+  if (e != hipSuccess) return bail(SPPO_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  const size_t delta_bytes = (size_t)p->batch * p->n_q_heads * c->s_max * sizeof(float);
+  e = hipMalloc(&c->delta, delta_bytes);
+  if (e != hipSuccess) {
+    c->delta = nullptr;
+    return bail(e == hipErrorOutOfMemory ? SPPO_ERR_OOM : SPPO_ERR_HIP,
+                std::string("hipMalloc(delta): ") + hipGetErrorString(e));
+  }
+  if ((e = hipStreamCreateWithFlags(&c->d2h, hipStreamNonBlocking)) != hipSuccess ||
+      (e = hipStreamCreateWithFlags(&c->h2d, hipStreamNonBlocking)) != hipSuccess) {
+    return bail(SPPO_ERR_HIP, std::string("hipStreamCreateWithFlags: ") + hipGetErrorString(e));
+  }
+  const int N = p->n_chunks;
+  for (auto* v : {&c->ev_fwd, &c->ev_off, &c->ev_call, &c->ev_pf}) {
+    v->assign(N, nullptr);
+    for (int i = 0; i < N; ++i) {
+      if ((e = hipEventCreateWithFlags(&(*v)[i], hipEventDisableTiming)) != hipSuccess) {
+        (*v)[i] = nullptr;
+        return bail(SPPO_ERR_HIP, std::string("hipEventCreate: ") + hipGetErrorString(e));
+      }
+    }
+  }
+  for (auto* v : {&c->t_d2h, &c->t_h2d}) {
+    v->assign(N, EventPair{});
+    for (int i = 0; i < N; ++i) {
+      if ((e = hipEventCreate(&(*v)[i].start)) != hipSuccess || (e = hipEventCreate(&(*v)[i].stop)) != hipSuccess) {
+        return bail(SPPO_ERR_HIP, std::string("hipEventCreate: ") + hipGetErrorString(e));
+      }
+    }
+  }
+  c->offloaded.assign(N, 0);
+  c->prefetched.assign(N, 0);
+  c->slots.assign(N, HostSlot{});
+  if (p->offload != SPPO_OFFLOAD_NONE) {
+    for (int i = 0; i < N; ++i) {
+      const size_t bq = bytes_q(c, i), bl = bytes_lse(c, i);
+      const size_t bkv = offload_kv(c) ? bytes_kv_row_block(c, i) * p->batch : 0;
+      auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+      const size_t total = 2 * up(bq) + up(bl) + 2 * up(bkv);
+      void* base = nullptr;
+      e = hipHostMalloc(&base, total, hipHostMallocDefault);
+      if (e != hipSuccess || !base) {
+        return bail(SPPO_ERR_OOM, "hipHostMalloc of " + std::to_string(total) + " pinned bytes for chunk " +
+                                      std::to_string(i) + " failed: " + hipGetErrorString(e));
+      }
+      HostSlot& s = c->slots[i];
+      char* b = static_cast<char*>(base);
+      s.base = base;
+      s.q = b;
+      s.o = b + up(bq);
+      s.lse = b + 2 * up(bq);
+      if (bkv) {
+        s.k = b + 2 * up(bq) + up(bl);
+        s.v = b + 2 * up(bq) + up(bl) + up(bkv);
+      }
+    }
+  }
+  *out = c;
+  return SPPO_OK;
+}
+
+sppo_status sppo_destroy(sppo_ctx* ctx) {
+  if (!ctx) return SPPO_OK;
+  destroy_all(ctx);
+  return SPPO_OK;
+}
+
+sppo_status sppo_get_offsets(const sppo_ctx* ctx, int64_t* out, int32_t capacity) {
+  if (!ctx || !out || capacity < ctx->prob.n_chunks + 1) return SPPO_ERR_INVALID_ARG;
+  for (int i = 0; i <= ctx->prob.n_chunks; ++i) out[i] = ctx->off[i];
+  return SPPO_OK;
+}
+
+sppo_status sppo_attn_fwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i, const void* k, const void* v,
+                                void* o_i, float* lse_i, void* stream) {
+  sppo_status st = check_ctx_index(ctx, i);
+  if (st != SPPO_OK) return st;
+  if ((st = check_ptr(ctx, q_i, "q_i")) || (st = check_ptr(ctx, k, "k")) || (st = check_ptr(ctx, v, "v")) ||
+      (st = check_ptr(ctx, o_i, "o_i")) || (st = check_ptr(ctx, lse_i, "lse_i"))) {
+    return st;
+  }
+  if (ctx->in_bwd || i != ctx->next_fwd) {
+    return fail(ctx, SPPO_ERR_ORDER, "forward of chunk " + std::to_string(i) + " out of order (expected " +
+                                         (ctx->in_bwd ? std::string("a backward call") : std::to_string(ctx->next_fwd)) + ")");
+  }
+  sppo::ChunkArgs a = make_args(ctx, i);
+  a.q = q_i;
+  a.k = k;
+  a.v = v;
+  a.o = o_i;
+  a.lse = lse_i;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf16 = ctx->prob.dtype == SPPO_BF16;
+  hipError_t e = timed_launch(ctx, SPPO_KERNEL_FWD, i, s, [&] {
+    return bf16 ? sppo::launch_fwd_bf16(a, s) : sppo::launch_fwd_f32(a, s);
+  });
+  if (e != hipSuccess) return hip_fail(ctx, e, "forward kernel launch");
+  if (i == 0) {
+    std::fill(ctx->offloaded.begin(), ctx->offloaded.end(), 0);
+    std::fill(ctx->prefetched.begin(), ctx->prefetched.end(), 0);
+  }
+  if (++ctx->next_fwd == ctx->prob.n_chunks) {
+    ctx->in_bwd = true;
+    ctx->next_bwd = ctx->prob.n_chunks - 1;
+  }
+  return SPPO_OK;
+}
+
+sppo_status sppo_attn_bwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i, const void* k, const void* v,
+                                const void* o_i, const float* lse_i, const void* do_i, void* dq_i,
+                                float* dk_acc, float* dv_acc, void* stream) {
+  sppo_status st = check_ctx_index(ctx, i);
+  if (st != SPPO_OK) return st;
+  if ((st = check_ptr(ctx, q_i, "q_i")) || (st = check_ptr(ctx, k, "k")) || (st = check_ptr(ctx, v, "v")) ||
+      (st = check_ptr(ctx, o_i, "o_i")) || (st = check_ptr(ctx, lse_i, "lse_i")) ||
+      (st = check_ptr(ctx, do_i, "do_i")) || (st = check_ptr(ctx, dq_i, "dq_i")) ||
+      (st = check_ptr(ctx, dk_acc, "dk_acc")) || (st = check_ptr(ctx, dv_acc, "dv_acc"))) {
+    return st;
+  }
+  if (!ctx->in_bwd || i != ctx->next_bwd) {
+    return fail(ctx, SPPO_ERR_ORDER, "backward of chunk " + std::to_string(i) + " out of order (expected " +
+                                         (ctx->in_bwd ? std::to_string(ctx->next_bwd) : std::string("the forward pass to finish")) + ")");
+  }
+  if (ctx->offloaded[i] && !ctx->prefetched[i]) {
+    return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " was offloaded but not prefetched");
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (ctx->prefetched[i]) SPPO_HIP(ctx, hipStreamWaitEvent(s, ctx->ev_pf[i], 0));
+  sppo::ChunkArgs a = make_args(ctx, i);
+  a.q = q_i;
+  a.k = k;
+  a.v = v;
+  a.o = const_cast<void*>(o_i);
+  a.lse = const_cast<float*>(lse_i);
+  a.dout = do_i;
+  a.dq = dq_i;
+  a.dk = dk_acc;
+  a.dv = dv_acc;
+  a.accumulate = (i == ctx->prob.n_chunks - 1) ? 0 : 1;
+  const bool bf16 = ctx->prob.dtype == SPPO_BF16;
+  hipError_t e = timed_launch(ctx, SPPO_KERNEL_BWD_PRE, i, s, [&] {
+    return bf16 ? sppo::launch_bwd_pre_bf16(a, s) : sppo::launch_bwd_pre_f32(a, s);
+  });
+  if (e == hipSuccess) {
+    e = timed_launch(ctx, SPPO_KERNEL_BWD_DKDV, i, s, [&] {
+      return bf16 ? sppo::launch_bwd_dkdv_bf16(a, s) : sppo::launch_bwd_dkdv_f32(a, s);
+    });
+  }
+  if (e == hipSuccess) {
+    e = timed_launch(ctx, SPPO_KERNEL_BWD_DQ, i, s, [&] {
+      return bf16 ? sppo::launch_bwd_dq_bf16(a, s) : sppo::launch_bwd_dq_f32(a, s);
+    });
+  }
+  if (e != hipSuccess) return hip_fail(ctx, e, "backward kernel launch");
+  if (--ctx->next_bwd < 0) {
+    ctx->in_bwd = false;
+    ctx->next_fwd = 0;
+  }
+  return SPPO_OK;
+}
+
+sppo_status sppo_offload_issue(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* src, void* stream) {
+  sppo_status st = check_ctx_index(ctx, i);
+  if (st != SPPO_OK) return st;
+  if (ctx->prob.offload == SPPO_OFFLOAD_NONE) return fail(ctx, SPPO_ERR_STATE, "context created with offload NONE");
+  if (!src) return fail(ctx, SPPO_ERR_INVALID_ARG, "null chunk buffers");
+  if ((st = check_ptr(ctx, src->q, "src.q")) || (st = check_ptr(ctx, src->o, "src.o")) ||
+      (st = check_ptr(ctx, src->lse, "src.lse"))) {
+    return st;
+  }
+  if (offload_kv(ctx) && ((st = check_ptr(ctx, src->k, "src.k")) || (st = check_ptr(ctx, src->v, "src.v")))) return st;
+  const bool fwd_done = ctx->in_bwd || i < ctx->next_fwd;
+  if (!fwd_done) return fail(ctx, SPPO_ERR_STATE, "offload of chunk " + std::to_string(i) + " before its forward");
+  if (ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " already offloaded");
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HostSlot& h = ctx->slots[i];
+  fold(ctx->t_d2h[i], ctx->ms_d2h);
+  SPPO_HIP(ctx, hipEventRecord(ctx->ev_fwd[i], s));
+  SPPO_HIP(ctx, hipStreamWaitEvent(ctx->d2h, ctx->ev_fwd[i], 0));
+  SPPO_HIP(ctx, hipEventRecord(ctx->t_d2h[i].start, ctx->d2h));
+  const size_t bq = bytes_q(ctx, i), bl = bytes_lse(ctx, i);
+  SPPO_HIP(ctx, hipMemcpyAsync(h.q, src->q, bq, hipMemcpyDeviceToHost, ctx->d2h));
+  SPPO_HIP(ctx, hipMemcpyAsync(h.o, src->o, bq, hipMemcpyDeviceToHost, ctx->d2h));
+  SPPO_HIP(ctx, hipMemcpyAsync(h.lse, src->lse, bl, hipMemcpyDeviceToHost, ctx->d2h));
+  uint64_t bytes = 2 * bq + bl;
+  if (offload_kv(ctx)) {
+    const size_t w = bytes_kv_row_block(ctx, i);
+    const size_t pitch = (size_t)ctx->prob.seq_len * ctx->prob.n_kv_heads * ctx->prob.head_dim * ctx->elt;
+    const size_t row_off = (size_t)ctx->off[i] * ctx->prob.n_kv_heads * ctx->prob.head_dim * ctx->elt;
+    const char* ks = static_cast<const char*>(src->k) + row_off;
+    const char* vs = static_cast<const char*>(src->v) + row_off;
+    if (ctx->prob.batch == 1) {
+      SPPO_HIP(ctx, hipMemcpyAsync(h.k, ks, w, hipMemcpyDeviceToHost, ctx->d2h));
+      SPPO_HIP(ctx, hipMemcpyAsync(h.v, vs, w, hipMemcpyDeviceToHost, ctx->d2h));
+    } else {
+      SPPO_HIP(ctx, hipMemcpy2DAsync(h.k, w, ks, pitch, w, ctx->prob.batch, hipMemcpyDeviceToHost, ctx->d2h));
+      SPPO_HIP(ctx, hipMemcpy2DAsync(h.v, w, vs, pitch, w, ctx->prob.batch, hipMemcpyDeviceToHost, ctx->d2h));
+    }
+    bytes += 2 * w * ctx->prob.batch;
+  }
+  SPPO_HIP(ctx, hipEventRecord(ctx->t_d2h[i].stop, ctx->d2h));
+  SPPO_HIP(ctx, hipEventRecord(ctx->ev_off[i], ctx->d2h));
+  ctx->t_d2h[i].pending = true;
+  ctx->offloaded[i] = 1;
+  ctx->prefetched[i] = 0;
+  ctx->bytes_d2h += bytes;
+  ctx->n_d2h += 1;
+  return SPPO_OK;
+}
+
+sppo_status sppo_offload_wait(sppo_ctx* ctx, int32_t i, void* stream) {
+  sppo_status st = check_ctx_index(ctx, i);
+  if (st != SPPO_OK) return st;
+  if (!ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " was not offloaded");
+  SPPO_HIP(ctx, hipStreamWaitEvent(static_cast<hipStream_t>(stream), ctx->ev_off[i], 0));
+  return SPPO_OK;
+}
+
+sppo_status sppo_prefetch(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* dst, void* stream) {
+  sppo_status st = check_ctx_index(ctx, i);
+  if (st != SPPO_OK) return st;
+  if (!dst) return fail(ctx, SPPO_ERR_INVALID_ARG, "null chunk buffers");
+  if ((st = check_ptr(ctx, dst->q, "dst.q")) || (st = check_ptr(ctx, dst->o, "dst.o")) ||
+      (st = check_ptr(ctx, dst->lse, "dst.lse"))) {
+    return st;
+  }
+  if (!ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "prefetch of chunk " + std::to_string(i) + " that was not offloaded");
+  if (ctx->prefetched[i]) return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " already prefetched");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HostSlot& h = ctx->slots[i];
+  fold(ctx->t_h2d[i], ctx->ms_h2d);
+  SPPO_HIP(ctx, hipEventRecord(ctx->ev_call[i], s));
+  SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_call[i], 0));
+  SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_off[i], 0));
+  SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d[i].start, ctx->h2d));
+  const size_t bq = bytes_q(ctx, i), bl = bytes_lse(ctx, i);
+  SPPO_HIP(ctx, hipMemcpyAsync(dst->q, h.q, bq, hipMemcpyHostToDevice, ctx->h2d));
+  SPPO_HIP(ctx, hipMemcpyAsync(dst->o, h.o, bq, hipMemcpyHostToDevice, ctx->h2d));
+  SPPO_HIP(ctx, hipMemcpyAsync(dst->lse, h.lse, bl, hipMemcpyHostToDevice, ctx->h2d));
+  SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d[i].stop, ctx->h2d));
+  SPPO_HIP(ctx, hipEventRecord(ctx->ev_pf[i], ctx->h2d));
+  ctx->t_h2d[i].pending = true;
+  ctx->prefetched[i] = 1;
+  ctx->bytes_h2d += 2 * bq + bl;
+  ctx->n_h2d += 1;
+  return SPPO_OK;
+}
+
+sppo_status sppo_reset(sppo_ctx* ctx) {
+  if (!ctx) return SPPO_ERR_INVALID_ARG;
+  ctx->in_bwd = false;
+  ctx->next_fwd = 0;
+  ctx->next_bwd = -1;
+  std::fill(ctx->offloaded.begin(), ctx->offloaded.end(), 0);
+  std::fill(ctx->prefetched.begin(), ctx->prefetched.end(), 0);
+  return SPPO_OK;
+}
+
+sppo_status sppo_set_kernel_timing(sppo_ctx* ctx, int32_t enable) {
+  if (!ctx) return SPPO_ERR_INVALID_ARG;
+  if (enable && ctx->t_kern[0].empty()) {
+    for (auto& v : ctx->t_kern) {
+      v.assign(ctx->prob.n_chunks, EventPair{});
+      for (EventPair& p : v) {
+        SPPO_HIP(ctx, hipEventCreate(&p.start));
+        SPPO_HIP(ctx, hipEventCreate(&p.stop));
+      }
+    }
+  }
+  ctx->ktiming = enable != 0;
+  return SPPO_OK;
+}
+
+sppo_status sppo_kernel_times(sppo_ctx* ctx, sppo_kernel_times_t* out, int32_t reset_after) {
+  if (!ctx || !out) return SPPO_ERR_INVALID_ARG;
+  for (int k = 0; k < SPPO_KERNEL_COUNT; ++k) {
+    for (EventPair& p : ctx->t_kern[k]) fold(p, ctx->kms[k]);
+    out->ms[k] = ctx->kms[k];
+    out->launches[k] = ctx->klaunch[k];
+    if (reset_after) {
+      ctx->kms[k] = 0.0;
+      ctx->klaunch[k] = 0;
+    }
+  }
+  return SPPO_OK;
+}
+
+sppo_status sppo_sync(sppo_ctx* ctx) {
+  if (!ctx) return SPPO_ERR_INVALID_ARG;
+  SPPO_HIP(ctx, hipStreamSynchronize(ctx->d2h));
+  SPPO_HIP(ctx, hipStreamSynchronize(ctx->h2d));
+  return SPPO_OK;
+}
+
+sppo_status sppo_copy_stats(sppo_ctx* ctx, sppo_copy_stats_t* out, int32_t reset_after) {
+  if (!ctx || !out) return SPPO_ERR_INVALID_ARG;
+  SPPO_HIP(ctx, hipStreamSynchronize(ctx->d2h));
+  SPPO_HIP(ctx, hipStreamSynchronize(ctx->h2d));
+  for (EventPair& p : ctx->t_d2h) fold(p, ctx->ms_d2h);
+  for (EventPair& p : ctx->t_h2d) fold(p, ctx->ms_h2d);
+  out->bytes_d2h = ctx->bytes_d2h;
+  out->bytes_h2d = ctx->bytes_h2d;
+  out->ms_d2h = ctx->ms_d2h;
+  out->ms_h2d = ctx->ms_h2d;
+  out->n_d2h = ctx->n_d2h;
+  out->n_h2d = ctx->n_h2d;
+  if (reset_after) {
+    ctx->bytes_d2h = ctx->bytes_h2d = 0;
+    ctx->ms_d2h = ctx->ms_h2d = 0.0;
+    ctx->n_d2h = ctx->n_h2d = 0;
+  }
+  return SPPO_OK;
+}
+
+}  // extern "C"

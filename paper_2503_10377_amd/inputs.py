@@ -1,0 +1,65 @@
+"""Seeded synthetic inputs for the chunked-attention path.
+
+Shared by the tests, ``__graft_entry__.smoke()`` and ``bench.py``; holds none
+of the attention arithmetic.  Values are i.i.d. N(0, 1) drawn in fp32 on the
+target device and rounded to the problem dtype (round-to-nearest-even for
+bf16).  Every block of 4096 rows of every tensor has its own seed derived
+from (seed, tensor, batch entry, block), so a tensor does not depend on how
+the sequence is chunked, and a prefix of a longer sequence is identical to
+the shorter one.
+
+Structured kinds exercise what random inputs cannot:
+    "randn"        Q, K, V, dO ~ N(0, 1)
+    "sharp_self"   Q[:, r, h] = 2 K[:, r, h // G]  (each row's own key dominates)
+    "sharp_future" Q[:, r, h] = 2 K[:, r+1, h // G] (the first invisible key
+                   dominates if the mask admits it; the last row uses its own key)
+    "zero_q"       Q = 0 (softmax is uniform over the visible keys)
+Multiplying by 2 is exact in bf16, so the structure survives the rounding.
+"""
+from __future__ import annotations
+
+import torch
+
+TENSOR_IDS = {"q": 0, "k": 1, "v": 2, "do": 3}
+BLOCK_ROWS = 4096
+KINDS = ("randn", "sharp_self", "sharp_future", "zero_q")
+
+
+def _block_seed(seed: int, tid: int, b: int, blk: int) -> int:
+    return (((seed & 0xFFFF) * 16 + tid) * 65536 + b) * (1 << 20) + blk
+
+
+def randn_bshd(shape, seed: int, tid: int, device, dtype) -> torch.Tensor:
+    """[B, S, H, D] tensor of N(0,1) draws rounded to ``dtype``, block-seeded."""
+    B, S, H, D = shape
+    out = torch.empty(shape, dtype=dtype, device=device)
+    gen = torch.Generator(device=device)
+    for b in range(B):
+        for r0 in range(0, S, BLOCK_ROWS):
+            r1 = min(S, r0 + BLOCK_ROWS)
+            gen.manual_seed(_block_seed(seed, tid, b, r0 // BLOCK_ROWS))
+            blk = torch.randn((r1 - r0, H, D), generator=gen, device=device, dtype=torch.float32)
+            out[b, r0:r1].copy_(blk.to(dtype))
+            del blk
+    return out
+
+
+def make_inputs(B: int, S: int, Hq: int, Hkv: int, D: int, dtype=torch.bfloat16, seed: int = 0,
+                device="cuda", kind: str = "randn") -> dict:
+    """Q, dO [B,S,Hq,D] and K, V [B,S,Hkv,D] on ``device``."""
+    if kind not in KINDS:
+        raise ValueError(f"unknown input kind {kind!r}")
+    G = Hq // Hkv
+    k = randn_bshd((B, S, Hkv, D), seed, TENSOR_IDS["k"], device, dtype)
+    v = randn_bshd((B, S, Hkv, D), seed, TENSOR_IDS["v"], device, dtype)
+    do = randn_bshd((B, S, Hq, D), seed, TENSOR_IDS["do"], device, dtype)
+    if kind == "randn":
+        q = randn_bshd((B, S, Hq, D), seed, TENSOR_IDS["q"], device, dtype)
+    elif kind == "zero_q":
+        q = torch.zeros((B, S, Hq, D), dtype=dtype, device=device)
+    else:
+        src = k
+        if kind == "sharp_future":
+            src = torch.cat([k[:, 1:], k[:, -1:]], dim=1)
+        q = (2 * src).repeat_interleave(G, dim=2).contiguous()
+    return {"q": q, "k": k, "v": v, "do": do}

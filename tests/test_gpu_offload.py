@@ -1,0 +1,159 @@
+"""Offload engine and C-ABI state machine on the GPU.
+
+* Offload must not change a single bit of any result (on/off equality), for
+  every offload mode, lookahead and offload set.
+* Poison test: once a chunk's copy has landed on the host its device
+  Q/O/LSE are overwritten with NaN; the backward must then read the
+  prefetched copies, so results stay bitwise equal (a read of stale or
+  not-yet-prefetched memory would surface as NaN).
+* Order/state violations return the documented status and enqueue nothing.
+"""
+import sys
+
+import pytest
+import torch
+
+from paper_2503_10377_amd import sppo as L
+from paper_2503_10377_amd.chunked import ChunkedAttention
+from paper_2503_10377_amd.inputs import make_inputs
+
+pytestmark = pytest.mark.gpu
+
+SHAPE = dict(B=1, S=4096, Hq=4, Hkv=2, D=128)
+N = 8
+
+
+def announce(msg):
+    print(f"\n[case] {msg}", file=sys.stderr, flush=True)
+
+
+def run(offload="none", offload_chunks=None, lookahead=2, poison=False, B=1, seed=0):
+    S, Hq, Hkv, D = SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"]
+    announce(f"offload={offload} chunks={offload_chunks} lookahead={lookahead} poison={poison} B={B}")
+    inp = make_inputs(B, S, Hq, Hkv, D, torch.bfloat16, seed=seed, device="cuda")
+    ca = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload=offload)
+    out = ca.alloc_outputs()
+    ca.step(inp, out, offload_chunks=offload_chunks, lookahead=lookahead, poison=poison)
+    torch.cuda.synchronize()
+    stats = L.sppo_copy_stats(ca.ctx) if offload != "none" else None
+    res = {"o": out["o"].clone(), "lse": ca.lse_full(out).clone(), "dq": out["dq"].clone(),
+           "dk": out["dk"].clone(), "dv": out["dv"].clone()}
+    ca.close()
+    return res, stats
+
+
+@pytest.fixture(scope="module")
+def baseline():
+    return run("none")[0]
+
+
+def assert_bitwise(a, b):
+    for n in a:
+        assert torch.equal(a[n], b[n]), n
+
+
+@pytest.mark.parametrize("mode", ["qol", "qkvol"])
+def test_offload_is_bitwise_invisible(baseline, mode):
+    res, stats = run(mode)
+    assert_bitwise(baseline, res)
+    assert stats["n_d2h"] == N - 1 and stats["n_h2d"] == N - 1
+    assert stats["ms_d2h"] > 0 and stats["ms_h2d"] > 0
+
+
+@pytest.mark.parametrize("lookahead", [0, 1, 3, 8])
+def test_poison_after_evict(baseline, lookahead):
+    res, _ = run("qkvol", offload_chunks=list(range(N)), lookahead=lookahead, poison=True)
+    assert_bitwise(baseline, res)
+
+
+def test_poison_batch2():
+    ref, _ = run("none", B=2, seed=3)
+    res, _ = run("qkvol", poison=True, B=2, seed=3)
+    assert_bitwise(ref, res)
+
+
+def test_copy_bytes_match_the_offload_set():
+    S, Hq, Hkv, D = SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"]
+    s = S // N
+    q_bytes = s * Hq * D * 2
+    lse_bytes = Hq * s * 4
+    kv_bytes = s * Hkv * D * 2
+    for mode, per_chunk_d2h in (("qol", 2 * q_bytes + lse_bytes),
+                                ("qkvol", 2 * q_bytes + lse_bytes + 2 * kv_bytes)):
+        _, stats = run(mode, offload_chunks=[0, 3, 5])
+        assert stats["bytes_d2h"] == 3 * per_chunk_d2h, mode
+        assert stats["bytes_h2d"] == 3 * (2 * q_bytes + lse_bytes), mode
+
+
+def test_order_and_state_errors():
+    S, Hq, Hkv, D = SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"]
+    announce("order and state errors")
+    inp = make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=0, device="cuda")
+    ca = ChunkedAttention(1, S, 4, Hq, Hkv, D, dtype="bf16", offload="qol")
+    out = ca.alloc_outputs()
+    q, k, v, do = inp["q"], inp["k"], inp["v"], inp["do"]
+    qc = [ca.chunk_view(q, i) for i in range(4)]
+    oc = [ca.chunk_view(out["o"], i) for i in range(4)]
+    dc = [ca.chunk_view(do, i) for i in range(4)]
+    dqc = [ca.chunk_view(out["dq"], i) for i in range(4)]
+    lse = out["lse"]
+    ctx = ca.ctx
+
+    def status_of(fn, *a):
+        try:
+            fn(*a)
+        except L.SppoError as e:
+            return e.status
+        return L.SPPO_OK
+
+    bufs = lambda i: L.chunk_bufs(q=qc[i], o=oc[i], lse=lse[i], k=k, v=v)  # noqa: E731
+    assert status_of(L.sppo_attn_fwd_chunk, ctx, 1, qc[1], k, v, oc[1], lse[1]) == L.SPPO_ERR_ORDER
+    assert status_of(L.sppo_attn_bwd_chunk, ctx, 3, qc[3], k, v, oc[3], lse[3], dc[3], dqc[3],
+                     out["dk"], out["dv"]) == L.SPPO_ERR_ORDER
+    assert status_of(L.sppo_offload_issue, ctx, 0, bufs(0)) == L.SPPO_ERR_STATE  # before its fwd
+    assert status_of(L.sppo_prefetch, ctx, 0, bufs(0)) == L.SPPO_ERR_STATE       # never offloaded
+    assert status_of(L.sppo_offload_wait, ctx, 0) == L.SPPO_ERR_STATE
+    assert status_of(L.sppo_attn_fwd_chunk, ctx, 7, qc[0], k, v, oc[0], lse[0]) == L.SPPO_ERR_INVALID_ARG
+    misaligned = qc[0].data_ptr() + 2
+    assert status_of(L.sppo_attn_fwd_chunk, ctx, 0, misaligned, k, v, oc[0], lse[0]) == L.SPPO_ERR_INVALID_ARG
+    assert L.sppo_last_error(ctx)
+    # A failed call leaves the context usable.
+    for i in range(4):
+        L.sppo_attn_fwd_chunk(ctx, i, qc[i], k, v, oc[i], lse[i])
+        if i < 2:
+            L.sppo_offload_issue(ctx, i, bufs(i))
+    assert status_of(L.sppo_offload_issue, ctx, 1, bufs(1)) == L.SPPO_ERR_STATE  # twice
+    assert status_of(L.sppo_attn_fwd_chunk, ctx, 0, qc[0], k, v, oc[0], lse[0]) == L.SPPO_ERR_ORDER
+    for i in (3, 2):
+        L.sppo_attn_bwd_chunk(ctx, i, qc[i], k, v, oc[i], lse[i], dc[i], dqc[i], out["dk"], out["dv"])
+    # chunk 1 was offloaded and not prefetched: its backward must refuse.
+    assert status_of(L.sppo_attn_bwd_chunk, ctx, 1, qc[1], k, v, oc[1], lse[1], dc[1], dqc[1],
+                     out["dk"], out["dv"]) == L.SPPO_ERR_STATE
+    L.sppo_prefetch(ctx, 1, bufs(1))
+    assert status_of(L.sppo_prefetch, ctx, 1, bufs(1)) == L.SPPO_ERR_STATE  # twice
+    L.sppo_attn_bwd_chunk(ctx, 1, qc[1], k, v, oc[1], lse[1], dc[1], dqc[1], out["dk"], out["dv"])
+    L.sppo_prefetch(ctx, 0, bufs(0))
+    L.sppo_attn_bwd_chunk(ctx, 0, qc[0], k, v, oc[0], lse[0], dc[0], dqc[0], out["dk"], out["dv"])
+    torch.cuda.synchronize()
+    assert torch.isfinite(out["dk"]).all() and torch.isfinite(out["dq"]).all()
+    # A new walk starts at fwd(0); reset abandons a partial walk.
+    L.sppo_attn_fwd_chunk(ctx, 0, qc[0], k, v, oc[0], lse[0])
+    L.sppo_reset(ctx)
+    L.sppo_attn_fwd_chunk(ctx, 0, qc[0], k, v, oc[0], lse[0])
+    L.sppo_sync(ctx)
+    torch.cuda.synchronize()
+    ca.close()
+
+
+def test_offload_on_context_without_offload_is_rejected():
+    S, Hq, Hkv, D = 256, 2, 2, 64
+    inp = make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=0, device="cuda")
+    ca = ChunkedAttention(1, S, 2, Hq, Hkv, D, dtype="bf16", offload="none")
+    out = ca.alloc_outputs()
+    L.sppo_attn_fwd_chunk(ca.ctx, 0, ca.chunk_view(inp["q"], 0), inp["k"], inp["v"],
+                          ca.chunk_view(out["o"], 0), out["lse"][0])
+    with pytest.raises(L.SppoError) as ei:
+        L.sppo_offload_issue(ca.ctx, 0, L.chunk_bufs(q=inp["q"], o=out["o"], lse=out["lse"][0]))
+    assert ei.value.status == L.SPPO_ERR_STATE
+    torch.cuda.synchronize()
+    ca.close()

@@ -1,0 +1,209 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times (same kernels, same chunking, same offload policy).
+
+The fp64 oracle cannot do whole tensors at 32K-1M tokens, so each size is
+checked on what it can compute one by one, plus properties that hold at any
+size:
+  * sampled query rows (O, LSE, dQ) at every chunk boundary, around the
+    first tile edges, mid-chunk, and at random, for whole KV-head groups;
+  * dK/dV of the last keys of the sequence (they only see the last rows);
+  * for 32K tokens, two complete heads against the full oracle;
+  * invariants of the exact gradient over the whole tensors, in fp64 on the
+    device: sum_j dK_j = 0, sum_j dV_j = sum_r dO_r (per KV group),
+    sum q.dQ = sum k.dK (per KV group).
+"""
+import concurrent.futures as cf
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2503_10377_amd.chunked import ChunkedAttention
+from paper_2503_10377_amd.inputs import make_inputs
+from parity import check
+
+pytestmark = pytest.mark.gpu
+
+THREADS = 8
+INV_TOL = 1e-3
+
+
+def announce(msg):
+    print(f"\n[case] {msg}", file=sys.stderr, flush=True)
+
+
+def sample_rows(offsets, S, n_random, rng, every=1):
+    rows = set()
+    for i in range(len(offsets) - 1):
+        c0, c1 = offsets[i], offsets[i + 1]
+        rows.update({c0, c1 - 1})
+        if i % every == 0:
+            rows.update({c0 + 1, c0 + 127, c0 + 128, (c0 + c1) // 2, c1 - 2})
+    rows.update(rng.integers(0, S, n_random).tolist())
+    return np.array(sorted(r for r in rows if 0 <= r < S))
+
+
+def host_rows(t, rows, heads):
+    idx = torch.as_tensor(rows, device=t.device)
+    return t[:, idx][:, :, heads].float().cpu().numpy().astype(np.float64)
+
+
+def host_group(t, g):
+    return t[:, :, g:g + 1].float().cpu().numpy()
+
+
+def run_full(S, N, Hq, Hkv, D, offload, seed=0):
+    announce(f"full size S={S} N={N} Hq={Hq} Hkv={Hkv} D={D} offload={offload}: inputs")
+    inp = make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=seed, device="cuda")
+    ca = ChunkedAttention(1, S, N, Hq, Hkv, D, dtype="bf16", offload=offload)
+    out = ca.alloc_outputs()
+    announce("HIP path: forward + backward walk")
+    ca.step(inp, out, lookahead=2)
+    torch.cuda.synchronize()
+    announce("HIP path done")
+    res = {"o": out["o"], "lse": ca.lse_full(out), "dq": out["dq"], "dk": out["dk"], "dv": out["dv"]}
+    for n, t in res.items():
+        assert torch.isfinite(t).all(), n
+    offsets = ca.offsets
+    ca.close()
+    return inp, res, offsets
+
+
+def check_sampled_rows(inp, res, offsets, groups, rows, Hq, Hkv, D):
+    G = Hq // Hkv
+    scale = 1 / math.sqrt(D)
+
+    def one(g):
+        heads = list(range(g * G, (g + 1) * G))
+        q = host_rows(inp["q"], rows, heads)
+        do = host_rows(inp["do"], rows, heads)
+        ref = oracle.rows_fwd_bwd(q, do, rows, host_group(inp["k"], g), host_group(inp["v"], g), scale)
+        got = {"o": host_rows(res["o"], rows, heads), "dq": host_rows(res["dq"], rows, heads),
+               "lse": res["lse"][:, heads][:, :, torch.as_tensor(rows, device="cuda")].cpu().numpy()}
+        return g, ref, got
+
+    announce(f"oracle: {len(rows)} rows x groups {list(groups)}")
+    worst = {}
+    with cf.ThreadPoolExecutor(THREADS) as ex:
+        for g, ref, got in ex.map(one, groups):
+            for n in ("o", "dq"):
+                r = check(f"{n}[g{g}]", got[n], ref[n], "bf16")
+                worst[n] = max(worst.get(n, 0), r["max_abs"])
+            r = check(f"lse[g{g}]", got["lse"], ref["lse"], "bf16", is_lse=True)
+            worst["lse"] = max(worst.get("lse", 0), r["max_abs"])
+    return worst
+
+
+def check_tail_keys(inp, res, groups, T, S, Hq, Hkv, D):
+    G = Hq // Hkv
+    scale = 1 / math.sqrt(D)
+    t0 = S - T
+
+    def one(g):
+        heads = list(range(g * G, (g + 1) * G))
+        rows = np.arange(t0, S)
+        dk, dv = oracle.tail_keys_bwd(host_rows(inp["q"], rows, heads), host_rows(inp["do"], rows, heads),
+                                      host_group(inp["k"], g), host_group(inp["v"], g), scale, t0)
+        return g, dk, dv
+
+    announce(f"oracle: last {T} keys x groups {list(groups)}")
+    with cf.ThreadPoolExecutor(THREADS) as ex:
+        for g, dk, dv in ex.map(one, groups):
+            check(f"dk_tail[g{g}]", res["dk"][:, t0:, g:g + 1].double().cpu().numpy(), dk, "bf16")
+            check(f"dv_tail[g{g}]", res["dv"][:, t0:, g:g + 1].double().cpu().numpy(), dv, "bf16")
+
+
+def check_invariants(inp, res, Hq, Hkv, block=65536):
+    """Exact-gradient identities over the whole tensors, accumulated in fp64
+    on the device over row blocks."""
+    announce("invariants")
+    G = Hq // Hkv
+    B, S = inp["q"].shape[:2]
+    f64 = dict(dtype=torch.float64, device="cuda")
+    sum_dk, sum_dv, sum_do = (torch.zeros(B, Hkv, inp["k"].shape[3], **f64) for _ in range(3))
+    mass_dk = torch.zeros(B, Hkv, **f64)
+    lhs, rhs, mass = (torch.zeros(B, Hkv, **f64) for _ in range(3))
+    for r0 in range(0, S, block):
+        r1 = min(S, r0 + block)
+        dk = res["dk"][:, r0:r1].double()
+        dv = res["dv"][:, r0:r1].double()
+        do = inp["do"][:, r0:r1].double()
+        sum_dk += dk.sum(dim=1)
+        mass_dk += dk.norm(dim=3).sum(dim=1)
+        sum_dv += dv.sum(dim=1)
+        sum_do += do.sum(dim=1).view(B, Hkv, G, -1).sum(dim=2)
+        qdq = (inp["q"][:, r0:r1].double() * res["dq"][:, r0:r1].double()).view(B, r1 - r0, Hkv, G, -1)
+        kdk = inp["k"][:, r0:r1].double() * dk
+        lhs += qdq.sum(dim=(1, 3, 4))
+        rhs += kdk.sum(dim=(1, 3))
+        mass += qdq.abs().sum(dim=(1, 3, 4)) + kdk.abs().sum(dim=(1, 3))
+        del dk, dv, do, qdq, kdk
+    assert (sum_dk.norm(dim=2) <= INV_TOL * mass_dk).all(), "sum_j dK_j != 0"
+    err = (sum_dv - sum_do).norm(dim=2)
+    assert (err <= INV_TOL * sum_do.norm(dim=2) + 1e-6 * S).all(), "sum_j dV_j != sum_r dO_r"
+    assert ((lhs - rhs).abs() <= INV_TOL * mass).all(), "sum q.dQ != sum k.dK"
+
+
+def test_seq32k_8chunks_no_offload():
+    """bf16, 32 heads x 128, seq 32768 in 8 chunks of 4096, no offload."""
+    S, N, Hq, Hkv, D = 32768, 8, 32, 32, 128
+    inp, res, off = run_full(S, N, Hq, Hkv, D, "none", seed=0)
+    rng = np.random.default_rng(1)
+    check_sampled_rows(inp, res, off, range(Hkv), sample_rows(off, S, 32, rng), Hq, Hkv, D)
+    check_invariants(inp, res, Hq, Hkv)
+    # Two complete heads (every row, every key) against the full oracle.
+    announce("oracle: full heads 0 and 31")
+    scale = 1 / math.sqrt(D)
+
+    def full_head(h):
+        sl = lambda t: t[:, :, h:h + 1].float().cpu().numpy()  # noqa: E731
+        return h, oracle.attention(sl(inp["q"]), sl(inp["k"]), sl(inp["v"]), sl(inp["do"]), scale)
+
+    with cf.ThreadPoolExecutor(2) as ex:
+        for h, ref in ex.map(full_head, (0, Hq - 1)):
+            got = {n: res[n][:, :, h:h + 1].double().cpu().numpy() for n in ("o", "dq", "dk", "dv")}
+            for n in got:
+                check(f"{n}[h{h}]", got[n], ref[n], "bf16", offsets=off, axis=1)
+            check(f"lse[h{h}]", res["lse"][:, h:h + 1].cpu().numpy(), ref["lse"], "bf16", is_lse=True)
+
+
+@pytest.mark.timeout(900)
+def test_seq128k_16chunks_offload():
+    """bf16, 32 heads x 128, seq 131072 in 16 chunks of 8192, Q/K/V/O/LSE
+    offloaded after each forward and prefetched before each backward."""
+    S, N, Hq, Hkv, D = 131072, 16, 32, 32, 128
+    inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=0)
+    rng = np.random.default_rng(2)
+    check_sampled_rows(inp, res, off, (0, Hkv - 1), sample_rows(off, S, 32, rng), Hq, Hkv, D)
+    check_sampled_rows(inp, res, off, range(Hkv), sample_rows(off[-2:], S, 4, rng), Hq, Hkv, D)
+    check_tail_keys(inp, res, (0, Hkv - 1), 512, S, Hq, Hkv, D)
+    check_invariants(inp, res, Hq, Hkv)
+
+
+@pytest.mark.timeout(1200)
+def test_seq512k_32chunks_gqa_offload():
+    """bf16 GQA, 32 query / 8 KV heads x 128, seq 524288 in 32 chunks of
+    16384, per-chunk offload/prefetch."""
+    S, N, Hq, Hkv, D = 524288, 32, 32, 8, 128
+    inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=0)
+    rng = np.random.default_rng(3)
+    check_sampled_rows(inp, res, off, (0, Hkv - 1), sample_rows(off, S, 16, rng, every=4), Hq, Hkv, D)
+    check_sampled_rows(inp, res, off, range(Hkv), np.array(sorted(rng.integers(0, S, 4))), Hq, Hkv, D)
+    check_tail_keys(inp, res, (0, Hkv - 1), 256, S, Hq, Hkv, D)
+    check_invariants(inp, res, Hq, Hkv)
+
+
+@pytest.mark.timeout(1800)
+def test_seq1m_64chunks_offload():
+    """bf16, 32 heads x 128, seq 1048576 in 64 chunks of 16384 (one GPU's
+    share of a multi-million-token sequence), full offload/prefetch walk."""
+    S, N, Hq, Hkv, D = 1048576, 64, 32, 32, 128
+    inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=0)
+    rng = np.random.default_rng(4)
+    check_sampled_rows(inp, res, off, (0, Hkv - 1), sample_rows(off, S, 16, rng, every=8), Hq, Hkv, D)
+    check_sampled_rows(inp, res, off, range(0, Hkv, 4), np.array(sorted(rng.integers(0, S, 2))), Hq, Hkv, D)
+    check_tail_keys(inp, res, (0, Hkv - 1), 128, S, Hq, Hkv, D)
+    check_invariants(inp, res, Hq, Hkv)

@@ -28,6 +28,14 @@ COMMON = [
     "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-function",
 ]
 
+# Per-source extra flags.  The forward keeps its MFMA accumulators in arch
+# VGPRs (the softmax reads S and rescales O with VALU ops, which would
+# otherwise shuttle them through AGPRs); it then fits 2 waves per SIMD.  The
+# backward kernels need more than 256 registers, so they keep the default.
+EXTRA = {
+    "attn_fwd_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
 
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
@@ -44,7 +52,7 @@ def sources() -> list[str]:
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [hipcc()] + COMMON + lang + ["-c", src, "-o", obj]
+    cmd = [hipcc()] + COMMON + EXTRA.get(os.path.basename(src), []) + lang + ["-c", src, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")

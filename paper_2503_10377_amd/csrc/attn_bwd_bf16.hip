@@ -6,7 +6,8 @@
 //   bwd_pre   Delta_r = <dO_r, O_r>                      (HBM-bound)
 //   bwd_dkdv  one workgroup per 128 keys of one KV head (4 waves x 32 keys,
 //             lane <-> key); streams the chunk's query tiles (64 rows, every
-//             query head of the GQA group) through LDS and accumulates
+//             query head of the GQA group) through LDS (natural, swizzled
+//             layout; Q^T and dO^T operands by transposed reads) and accumulates
 //               dV += P^T dO,  dK += scale * dS^T Q
 //             in registers; S = Q K^T and dP = dO V^T are recomputed.
 //   bwd_dq    one workgroup per 128 query rows of one head (lane <-> query);
@@ -55,13 +56,12 @@ __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(ChunkArgs a) {
 template <int D>
 __global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
   constexpr int BR = kDqBR, BC = kDqBC;
-  constexpr int KP = D + 8, TP = BC + 4;
-  constexpr int NK = D / 16, ND = D / 32, CG = D / 8;
+  using T = LdsTile<D>;
+  constexpr int NK = D / 16, ND = D / 32, CG = T::CG;
   constexpr int ITEMS = (BC / 4) * CG;
   constexpr int IPT = (ITEMS + 255) / 256;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BC * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[BC * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t Kt[D * TP];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[BC * T::P];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[BC * T::P];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, g = lane >> 5;
@@ -76,6 +76,7 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
   const int64_t kend = (q0 + BR < c1) ? q0 + BR : c1;
   const int nkv = (int)((kend + BC - 1) / BC);
   const float C = a.scale * kLog2e;
+  const int nat = T::nat_base(lane), trb = T::tr_base(lane);
 
   bf16x8 qf[NK], df[NK];
   float lse2 = INFINITY, dl = 0.f;
@@ -126,42 +127,40 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
       const int c = tid + 256 * u;
       if (ITEMS % 256 == 0 || c < ITEMS) {
         const int rg = c / CG, cg = c % CG;
-        store_block_nat(kreg[u], Ks, KP, 4 * rg, 8 * cg);
-        store_block_trans(kreg[u], Kt, TP, 4 * rg, 8 * cg);
-        store_block_nat(vreg[u], Vs, KP, 4 * rg, 8 * cg);
+        store_block_tile<D>(kreg[u], Ks, rg, cg);
+        store_block_tile<D>(vreg[u], Vs, rg, cg);
       }
     }
     __syncthreads();
     if (it + 1 < nkv) load_tile(it + 1);
 
     const bool need_mask = k0 + BC - 1 > q0 + 32 * w;
+    const int rel = (int)(r - k0);
     bf16x8 dsb[4];
 #pragma unroll
     for (int jb = 0; jb < 2; ++jb) {
       f32x16 sv = f32x16{}, dp = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < NK; ++kk) {
-        sv = mfma32(ld_lds16(Ks + (32 * jb + l32) * KP + 16 * kk + 8 * g), qf[kk], sv);
-        dp = mfma32(ld_lds16(Vs + (32 * jb + l32) * KP + 16 * kk + 8 * g), df[kk], dp);
+        sv = mfma32(ld_lds_nat<D>(Ks, nat, 32 * jb, kk), qf[kk], sv);
+        dp = mfma32(ld_lds_nat<D>(Vs, nat, 32 * jb, kk), df[kk], dp);
       }
       float ds[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         float p = fast_exp2(sv[v] * C - lse2);
-        if (need_mask) {
-          const int64_t key = k0 + 32 * jb + 8 * (v / 4) + 4 * g + (v % 4);
-          if (key > r) p = 0.f;
-        }
+        if (need_mask && 32 * jb + 8 * (v / 4) + 4 * g + (v % 4) > rel) p = 0.f;
         ds[v] = p * (dp[v] - dl);
       }
       dsb[2 * jb] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
       dsb[2 * jb + 1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
     }
+    // dQ^T[d][query] += K^T dS^T: K^T comes from transposed reads of K.
 #pragma unroll
     for (int db = 0; db < ND; ++db) {
 #pragma unroll
       for (int kb = 0; kb < BC / 16; ++kb) {
-        dq[db] = mfma32(ld_lds_perm(Kt + (32 * db + l32) * TP + 16 * kb + 4 * g), dsb[kb], dq[db]);
+        dq[db] = mfma32(ld_lds_tr<D>(Ks, trb, 16 * kb, 32 * db), dsb[kb], dq[db]);
       }
     }
   }
@@ -172,13 +171,9 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
     for (int db = 0; db < ND; ++db) {
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
-        bf16x2 lo, hi;
-        lo.x = (__bf16)(dq[db][4 * q4 + 0] * a.scale);
-        lo.y = (__bf16)(dq[db][4 * q4 + 1] * a.scale);
-        hi.x = (__bf16)(dq[db][4 * q4 + 2] * a.scale);
-        hi.y = (__bf16)(dq[db][4 * q4 + 3] * a.scale);
-        u32x2 wv = {__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
-        *reinterpret_cast<u32x2*>(qrow + 32 * db + 8 * q4 + 4 * g) = wv;
+        *reinterpret_cast<u32x2*>(qrow + 32 * db + 8 * q4 + 4 * g) =
+            pack_bf16x4(dq[db][4 * q4 + 0] * a.scale, dq[db][4 * q4 + 1] * a.scale,
+                        dq[db][4 * q4 + 2] * a.scale, dq[db][4 * q4 + 3] * a.scale);
       }
     }
   }
@@ -188,14 +183,12 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
 template <int D>
 __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   constexpr int BQ = kKvBQ;
-  constexpr int KP = D + 8, TQ = BQ + 4;
-  constexpr int NK = D / 16, ND = D / 32, CG = D / 8;
+  using T = LdsTile<D>;
+  constexpr int NK = D / 16, ND = D / 32, CG = T::CG;
   constexpr int ITEMS = (BQ / 4) * CG;
   constexpr int IPT = (ITEMS + 255) / 256;
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[BQ * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t Ds[BQ * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t Qt[D * TQ];
-  __shared__ __attribute__((aligned(16))) uint16_t Dt[D * TQ];
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[BQ * T::P];
+  __shared__ __attribute__((aligned(16))) uint16_t Ds[BQ * T::P];
   __shared__ __attribute__((aligned(16))) float lse2s[BQ];
   __shared__ __attribute__((aligned(16))) float dls[BQ];
 
@@ -208,6 +201,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   const int64_t k0 = (int64_t)blockIdx.x * kKvBKV;
   const int64_t j = k0 + 32 * w + l32;  // this lane's key
   const float C = a.scale * kLog2e;
+  const int nat = T::nat_base(lane), trb = T::tr_base(lane);
 
   bf16x8 kf[NK], vf[NK];
   {
@@ -269,10 +263,8 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
       const int c = tid + 256 * u;
       if (ITEMS % 256 == 0 || c < ITEMS) {
         const int rg = c / CG, cg = c % CG;
-        store_block_nat(qreg[u], Qs, KP, 4 * rg, 8 * cg);
-        store_block_trans(qreg[u], Qt, TQ, 4 * rg, 8 * cg);
-        store_block_nat(dreg[u], Ds, KP, 4 * rg, 8 * cg);
-        store_block_trans(dreg[u], Dt, TQ, 4 * rg, 8 * cg);
+        store_block_tile<D>(qreg[u], Qs, rg, cg);
+        store_block_tile<D>(dreg[u], Ds, rg, cg);
       }
     }
     if (tid < BQ) {
@@ -288,10 +280,11 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
       f32x16 sv = f32x16{}, dp = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < NK; ++kk) {
-        sv = mfma32(ld_lds16(Qs + (32 * ib + l32) * KP + 16 * kk + 8 * g), kf[kk], sv);
-        dp = mfma32(ld_lds16(Ds + (32 * ib + l32) * KP + 16 * kk + 8 * g), vf[kk], dp);
+        sv = mfma32(ld_lds_nat<D>(Qs, nat, 32 * ib, kk), kf[kk], sv);
+        dp = mfma32(ld_lds_nat<D>(Ds, nat, 32 * ib, kk), vf[kk], dp);
       }
       const bool need_mask = k0 + 32 * w + 31 > q0 + 32 * ib;
+      const int rel = (int)(j - q0);  // this lane's key relative to the query tile
       float p[16], ds[16];
 #pragma unroll
       for (int v4 = 0; v4 < 4; ++v4) {
@@ -304,7 +297,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
         for (int e = 0; e < 4; ++e) {
           const int v = 4 * v4 + e;
           float pv = fast_exp2(sv[v] * C - lv[e]);
-          if (need_mask && j > q0 + qi + e) pv = 0.f;
+          if (need_mask && rel > qi + e) pv = 0.f;
           p[v] = pv;
           ds[v] = pv * (dp[v] - dv4[e]);
         }
@@ -320,8 +313,8 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
           const int kb = 2 * ib + hh;
-          dv[db] = mfma32(pb[hh], ld_lds_perm(Dt + (32 * db + l32) * TQ + 16 * kb + 4 * g), dv[db]);
-          dk[db] = mfma32(dsb[hh], ld_lds_perm(Qt + (32 * db + l32) * TQ + 16 * kb + 4 * g), dk[db]);
+          dv[db] = mfma32(pb[hh], ld_lds_tr<D>(Ds, trb, 16 * kb, 32 * db), dv[db]);
+          dk[db] = mfma32(dsb[hh], ld_lds_tr<D>(Qs, trb, 16 * kb, 32 * db), dk[db]);
         }
       }
     }

@@ -6,8 +6,9 @@
 // Sec. 5.1 of SPPO: K/V of all earlier subsequences stay resident on the GPU).
 //
 // One workgroup = 4 waves = 128 query rows of one head; each wave owns 32
-// rows.  K/V tiles of 64 keys are staged through LDS (K natural, V
-// transposed), prefetched into registers one tile ahead.  Per tile each wave
+// rows.  K/V tiles of 64 keys are staged through LDS in natural layout
+// (swizzled, conflict-free), prefetched into registers one tile ahead; V^T
+// operands come from ds_read_b64_tr_b16 transposed reads.  Per tile each wave
 //   S^T[key][query] = K Q^T          (16x v_mfma_f32_32x32x16_bf16, D=128)
 //   online softmax in base 2 (lane <-> query, so row statistics are in-lane
 //   plus one exchange with lane^32)
@@ -21,19 +22,19 @@ namespace {
 
 constexpr int kFwdBR = 128;  // query rows per workgroup (4 waves x 32)
 constexpr int kFwdBC = 64;   // keys per K/V tile
+constexpr float kLazyMax = 8.f;  // log2 headroom before the running max moves
 
 template <int D>
 __global__ __launch_bounds__(256) void fwd_bf16_kernel(ChunkArgs a) {
   constexpr int BR = kFwdBR, BC = kFwdBC;
-  constexpr int KP = D + 8;   // natural tile pitch (elements); rows 16B aligned
-  constexpr int TP = BC + 4;  // transposed tile pitch; rows 8B aligned
+  using T = LdsTile<D>;
   constexpr int NK = D / 16;  // k-steps of K Q^T
   constexpr int ND = D / 32;  // 32-wide d blocks of O^T
-  constexpr int CG = D / 8;   // 8-column groups per row
+  constexpr int CG = T::CG;
   constexpr int ITEMS = (BC / 4) * CG;
   constexpr int IPT = (ITEMS + 255) / 256;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BC * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * TP];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[BC * T::P];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[BC * T::P];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, g = lane >> 5;
@@ -48,6 +49,7 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(ChunkArgs a) {
   const int64_t kend = (q0 + BR < c1) ? q0 + BR : c1;
   const int nkv = (int)((kend + BC - 1) / BC);
   const float C = a.scale * kLog2e;
+  const int nat = T::nat_base(lane), trb = T::tr_base(lane);
 
   bf16x8 qf[NK];
   {
@@ -90,8 +92,8 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(ChunkArgs a) {
       const int c = tid + 256 * u;
       if (ITEMS % 256 == 0 || c < ITEMS) {
         const int rg = c / CG, cg = c % CG;
-        store_block_nat(kreg[u], Ks, KP, 4 * rg, 8 * cg);
-        store_block_trans(vreg[u], Vt, TP, 4 * rg, 8 * cg);
+        store_block_tile<D>(kreg[u], Ks, rg, cg);
+        store_block_tile<D>(vreg[u], Vs, rg, cg);
       }
     }
     __syncthreads();
@@ -104,55 +106,61 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(ChunkArgs a) {
       sv[jb] = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < NK; ++kk) {
-        sv[jb] = mfma32(ld_lds16(Ks + (32 * jb + l32) * KP + 16 * kk + 8 * g), qf[kk], sv[jb]);
+        sv[jb] = mfma32(ld_lds_nat<D>(Ks, nat, 32 * jb, kk), qf[kk], sv[jb]);
       }
     }
     // Causal mask: only tiles that reach past the wave's first row need it.
     if (k0 + BC - 1 > q0 + 32 * w) {
+      const int rel = (int)(r - k0);  // key offset within the tile of this row
 #pragma unroll
       for (int jb = 0; jb < 2; ++jb) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int64_t key = k0 + 32 * jb + 8 * (v / 4) + 4 * g + (v % 4);
-          if (key > r) sv[jb][v] = -INFINITY;
+          if (32 * jb + 8 * (v / 4) + 4 * g + (v % 4) > rel) sv[jb][v] = -INFINITY;
         }
       }
     }
-    // Online softmax, base 2: x = s * scale * log2(e).
+  // Online softmax, base 2: x = s * scale * log2(e).  The running max m
+    // is only moved when some row of the wave sees a tile max more than
+    // kLazyMax above it (then O and l are rescaled); otherwise the stale m
+    // is kept, so P = exp2(x - m) stays <= 2^kLazyMax -- exact in fp32, and
+    // in range for bf16 -- and the 64-register O rescale is skipped.
     float mx = -INFINITY;
 #pragma unroll
     for (int jb = 0; jb < 2; ++jb) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sv[jb][v]);
     }
-    mx = fmaxf(mx, xor32(mx));
-    const float mnew = fmaxf(m, mx * C);
-    const float alpha = (mnew == -INFINITY) ? 1.f : fast_exp2(m - mnew);
-    m = mnew;
-    lsum *= alpha;
+    mx = fmaxf(mx, xor32(mx)) * C;
+    if (__any(mx > m + kLazyMax)) {
+      const float mnew = fmaxf(m, mx);
+      const float alpha = fast_exp2(m - mnew);  // m = -inf on the first tile: 0
+      m = mnew;
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < ND; ++db) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+      }
+    }
     bf16x8 pb[4];
 #pragma unroll
     for (int jb = 0; jb < 2; ++jb) {
       float p[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        p[v] = fast_exp2(sv[jb][v] * C - mnew);
+        p[v] = fast_exp2(sv[jb][v] * C - m);
         lsum += p[v];
       }
       pb[2 * jb] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
       pb[2 * jb + 1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
-    }
-#pragma unroll
-    for (int db = 0; db < ND; ++db) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
     }
     // O^T += V^T P^T.
 #pragma unroll
     for (int db = 0; db < ND; ++db) {
 #pragma unroll
       for (int kb = 0; kb < BC / 16; ++kb) {
-        o[db] = mfma32(ld_lds_perm(Vt + (32 * db + l32) * TP + 16 * kb + 4 * g), pb[kb], o[db]);
+        o[db] = mfma32(ld_lds_tr<D>(Vs, trb, 16 * kb, 32 * db), pb[kb], o[db]);
       }
     }
   }
@@ -165,13 +173,9 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(ChunkArgs a) {
     for (int db = 0; db < ND; ++db) {
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
-        bf16x2 lo, hi;
-        lo.x = (__bf16)(o[db][4 * q4 + 0] * inv);
-        lo.y = (__bf16)(o[db][4 * q4 + 1] * inv);
-        hi.x = (__bf16)(o[db][4 * q4 + 2] * inv);
-        hi.y = (__bf16)(o[db][4 * q4 + 3] * inv);
-        u32x2 wv = {__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
-        *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * q4 + 4 * g) = wv;
+        *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * q4 + 4 * g) =
+            pack_bf16x4(o[db][4 * q4 + 0] * inv, o[db][4 * q4 + 1] * inv, o[db][4 * q4 + 2] * inv,
+                        o[db][4 * q4 + 3] * inv);
       }
     }
     if (g == 0) a.lse[(b * a.Hq + h) * s + (r - c0)] = (m + fast_log2(lt)) * kLn2;

@@ -22,6 +22,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -141,6 +142,28 @@ sppo::ChunkArgs make_args(const sppo_ctx* c, int i) {
   a.scale = c->scale;
   a.delta = c->delta;
   return a;
+}
+
+// Device->host copy of n contiguous bytes.  Issued as rect copies (rows of
+// 1 MiB plus a tail row) because the runtime serves those with the SDMA
+// engines, whereas a linear device->host hipMemcpyAsync is served by a blit
+// kernel that must find free compute units next to the attention kernels.
+bool g_d2h_rect = [] {
+  const char* e = getenv("SPPO_D2H_RECT");
+  return !(e && e[0] == '0');
+}();
+
+hipError_t copy_d2h(void* dst, const void* src, size_t n, hipStream_t s) {
+  if (!g_d2h_rect) return hipMemcpyAsync(dst, src, n, hipMemcpyDeviceToHost, s);
+  constexpr size_t W = size_t(1) << 20;
+  const size_t rows = n / W, tail = n % W;
+  hipError_t e = hipSuccess;
+  if (rows) e = hipMemcpy2DAsync(dst, W, src, W, W, rows, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess && tail) {
+    e = hipMemcpy2DAsync(static_cast<char*>(dst) + rows * W, tail, static_cast<const char*>(src) + rows * W,
+                         tail, tail, 1, hipMemcpyDeviceToHost, s);
+  }
+  return e;
 }
 
 // Fold a finished timing pair into the totals (waits for it if needed).
@@ -448,9 +471,9 @@ sppo_status sppo_offload_issue(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* 
   SPPO_HIP(ctx, hipStreamWaitEvent(ctx->d2h, ctx->ev_fwd[i], 0));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_d2h[i].start, ctx->d2h));
   const size_t bq = bytes_q(ctx, i), bl = bytes_lse(ctx, i);
-  SPPO_HIP(ctx, hipMemcpyAsync(h.q, src->q, bq, hipMemcpyDeviceToHost, ctx->d2h));
-  SPPO_HIP(ctx, hipMemcpyAsync(h.o, src->o, bq, hipMemcpyDeviceToHost, ctx->d2h));
-  SPPO_HIP(ctx, hipMemcpyAsync(h.lse, src->lse, bl, hipMemcpyDeviceToHost, ctx->d2h));
+  SPPO_HIP(ctx, copy_d2h(h.q, src->q, bq, ctx->d2h));
+  SPPO_HIP(ctx, copy_d2h(h.o, src->o, bq, ctx->d2h));
+  SPPO_HIP(ctx, copy_d2h(h.lse, src->lse, bl, ctx->d2h));
   uint64_t bytes = 2 * bq + bl;
   if (offload_kv(ctx)) {
     const size_t w = bytes_kv_row_block(ctx, i);
@@ -459,8 +482,8 @@ sppo_status sppo_offload_issue(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* 
     const char* ks = static_cast<const char*>(src->k) + row_off;
     const char* vs = static_cast<const char*>(src->v) + row_off;
     if (ctx->prob.batch == 1) {
-      SPPO_HIP(ctx, hipMemcpyAsync(h.k, ks, w, hipMemcpyDeviceToHost, ctx->d2h));
-      SPPO_HIP(ctx, hipMemcpyAsync(h.v, vs, w, hipMemcpyDeviceToHost, ctx->d2h));
+      SPPO_HIP(ctx, copy_d2h(h.k, ks, w, ctx->d2h));
+      SPPO_HIP(ctx, copy_d2h(h.v, vs, w, ctx->d2h));
     } else {
       SPPO_HIP(ctx, hipMemcpy2DAsync(h.k, w, ks, pitch, w, ctx->prob.batch, hipMemcpyDeviceToHost, ctx->d2h));
       SPPO_HIP(ctx, hipMemcpy2DAsync(h.v, w, vs, pitch, w, ctx->prob.batch, hipMemcpyDeviceToHost, ctx->d2h));

@@ -1,6 +1,6 @@
 // Device-side helpers shared by the gfx950 attention kernels: vector types,
-// bf16 MFMA wrappers, global->register tile loads and register->LDS stores in
-// natural ([row][col]) and transposed ([col][row]) layouts.
+// the bf16 MFMA wrapper, global->register tile loads, and the swizzled LDS
+// tile layout with its natural and transposed operand reads.
 //
 // MFMA register layout used throughout (v_mfma_f32_32x32x16_bf16, wave64):
 //   A[i][k] : lane l holds row i = l%32 and 8 k-values in "k-slots"
@@ -26,6 +26,8 @@ typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(4))) short v4i16;
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -38,19 +40,6 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& x) { return __builtin_b
 
 __device__ __forceinline__ u32x4 ld_global16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 
-__device__ __forceinline__ bf16x8 ld_lds16(const uint16_t* p) {
-  return as_bf16x8(*reinterpret_cast<const u32x4*>(p));
-}
-
-// Two 8-byte LDS reads (k-slots 0..3 at p, 4..7 at p+8 elements) of a
-// transposed tile: the permuted k-slot map described above.
-__device__ __forceinline__ bf16x8 ld_lds_perm(const uint16_t* p) {
-  u32x2 lo = *reinterpret_cast<const u32x2*>(p);
-  u32x2 hi = *reinterpret_cast<const u32x2*>(p + 8);
-  u32x4 r = {lo.x, lo.y, hi.x, hi.y};
-  return as_bf16x8(r);
-}
-
 // Round 8 floats to bf16 (round-to-nearest-even, v_cvt_pk_bf16_f32).
 __device__ __forceinline__ bf16x8 pack_bf16x8(float x0, float x1, float x2, float x3, float x4,
                                               float x5, float x6, float x7) {
@@ -60,11 +49,12 @@ __device__ __forceinline__ bf16x8 pack_bf16x8(float x0, float x1, float x2, floa
   return r;
 }
 
-// Pack C-tile values v0..v0+7 of a 32x32 accumulator into one bf16x8 operand
-// (k-slot e <- value v0 + e).
-__device__ __forceinline__ bf16x8 pack_c8(const f32x16& c, int v0) {
-  return pack_bf16x8(c[v0 + 0], c[v0 + 1], c[v0 + 2], c[v0 + 3], c[v0 + 4], c[v0 + 5], c[v0 + 6],
-                     c[v0 + 7]);
+// Four fp32 values rounded to bf16 as two packed dwords.
+__device__ __forceinline__ u32x2 pack_bf16x4(float x0, float x1, float x2, float x3) {
+  bf16x2 lo, hi;
+  lo.x = (__bf16)x0; lo.y = (__bf16)x1;
+  hi.x = (__bf16)x2; hi.y = (__bf16)x3;
+  return u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -72,53 +62,89 @@ __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_lo
 
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
 
-// A 4-row x 8-column bf16 block held by one thread: rows r0..r0+3 of a tile,
-// columns c0..c0+7, as four 16-byte words.
+// ------------------------------------------------------ global tile loads
+// A 4-row x 8-column bf16 block held by one thread as four 16-byte words.
 struct Block4x8 {
   u32x4 r[4];
 };
 
-// Load rows [row0, row0+4) x cols [col0, col0+8) of a row-major bf16 matrix
-// whose row `x` starts at base + x*row_stride; rows >= row_limit read as 0.
+// Rows [row0, row0+4) x cols [col0, col0+8) of a row-major bf16 matrix
+// whose row x starts at base + x*row_stride; rows >= row_limit read as 0.
 __device__ __forceinline__ void load_block4x8(Block4x8& blk, const uint16_t* base, int64_t row_stride,
                                               int64_t row0, int64_t row_limit, int col0) {
+  const uint16_t* p = base + row0 * row_stride + col0;
+  if (row0 + 4 <= row_limit) {
 #pragma unroll
-  for (int x = 0; x < 4; ++x) {
-    const int64_t row = row0 + x;
-    if (row < row_limit) {
-      blk.r[x] = ld_global16(base + row * row_stride + col0);
-    } else {
-      blk.r[x] = u32x4{0u, 0u, 0u, 0u};
+    for (int x = 0; x < 4; ++x) blk.r[x] = ld_global16(p + x * row_stride);
+  } else {
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      blk.r[x] = (row0 + x < row_limit) ? ld_global16(p + x * row_stride) : u32x4{0u, 0u, 0u, 0u};
     }
   }
 }
 
-// Store the block in natural layout: lds[(row)*pitch + col].
-__device__ __forceinline__ void store_block_nat(const Block4x8& blk, uint16_t* lds, int pitch, int row0,
-                                                int col0) {
+// ---------------------------------------------------------------- LDS tiles
+// A bf16 tile [rows][D] in LDS is stored in natural layout (row = key or
+// query, column = head dim) with row pitch D + 16 elements, and the 16-byte
+// chunk index of row r XOR-ed with bit 2 of r.  For D = 128 this makes all
+// three access patterns free of bank conflicts on the 32-bank LDS: the 4x8
+// block stores, the natural MFMA-operand reads (rows l%32, 16-byte chunks),
+// and the ds_read_b64_tr_b16 transposed reads.  Every swizzle term is a
+// per-lane constant, so each access is a lane base plus an immediate.
+template <int D>
+struct LdsTile {
+  static constexpr int P = D + 16;
+  static constexpr int CG = D / 8;  // 16-byte chunks per row
+  // Element offset of row 4*rg + x, 16-byte chunk cg.
+  static __device__ __forceinline__ int store_off(int rg, int x, int cg) {
+    return (4 * rg + x) * P + 8 * (cg ^ (rg & 1));
+  }
+  // Lane base of a natural operand read: row l%32, chunk 2*kk + l/32 (add
+  // rb*P + 16*kk for row block rb, rb % 32 == 0, and k-step kk).
+  static __device__ __forceinline__ int nat_base(int lane) {
+    const int l32 = lane & 31, g = lane >> 5;
+    return l32 * P + 8 * (g ^ ((l32 >> 2) & 1));
+  }
+  // Lane base of a transposed read (add (k0 + {0,8})*P + x0 with k0 % 16 == 0
+  // and x0 % 32 == 0).  Source lane s = 16q + 4e + a supplies the 8 bytes at
+  // row 4*(q/2) + e, column 16*(q%2) + 4*a; ds_read_b64_tr_b16 hands output
+  // lane 16q + 4a' + b element b of source lanes 16q + 4e + a', e = 0..3.
+  static __device__ __forceinline__ int tr_base(int lane) {
+    const int q = lane >> 4, e = (lane >> 2) & 3, a = lane & 3;
+    return (4 * (q >> 1) + e) * P + 8 * ((2 * (q & 1) + (a >> 1)) ^ ((q >> 1) & 1)) + 4 * (a & 1);
+  }
+};
+
+template <int D>
+__device__ __forceinline__ void store_block_tile(const Block4x8& blk, uint16_t* tile, int rg, int cg) {
 #pragma unroll
   for (int x = 0; x < 4; ++x) {
-    *reinterpret_cast<u32x4*>(lds + (row0 + x) * pitch + col0) = blk.r[x];
+    *reinterpret_cast<u32x4*>(tile + LdsTile<D>::store_off(rg, x, cg)) = blk.r[x];
   }
 }
 
-// Store the block transposed: lds[(col)*pitch + row], 4 consecutive rows of
-// one column forming one 8-byte word.
-__device__ __forceinline__ void store_block_trans(const Block4x8& blk, uint16_t* lds, int pitch,
-                                                  int row0, int col0) {
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int w = e >> 1;
-    uint32_t lo, hi;
-    if (e & 1) {
-      lo = (blk.r[0][w] >> 16) | (blk.r[1][w] & 0xffff0000u);
-      hi = (blk.r[2][w] >> 16) | (blk.r[3][w] & 0xffff0000u);
-    } else {
-      lo = (blk.r[0][w] & 0xffffu) | (blk.r[1][w] << 16);
-      hi = (blk.r[2][w] & 0xffffu) | (blk.r[3][w] << 16);
-    }
-    *reinterpret_cast<u32x2*>(lds + (col0 + e) * pitch + row0) = u32x2{lo, hi};
-  }
+// Natural operand: lane l gets row rb + l%32, columns 16*kk + 8*(l/32) + 0..7.
+template <int D>
+__device__ __forceinline__ bf16x8 ld_lds_nat(const uint16_t* tile, int nat_base, int rb, int kk) {
+  return as_bf16x8(*reinterpret_cast<const u32x4*>(tile + nat_base + rb * LdsTile<D>::P + 16 * kk));
+}
+
+__device__ __forceinline__ v4i16 ds_read_tr16(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
+}
+
+// Transposed operand from a natural tile: lane l gets column x0 + l%32 and
+// rows k0 + {8*(e/4) + 4*(l/32) + e%4 : e = 0..7}, i.e. the permuted k-slot
+// map, so it pairs with an operand taken from C-tile registers.
+template <int D>
+__device__ __forceinline__ bf16x8 ld_lds_tr(const uint16_t* tile, int tr_base, int k0, int x0) {
+  constexpr int P = LdsTile<D>::P;
+  const v4i16 lo = ds_read_tr16(tile + tr_base + k0 * P + x0);
+  const v4i16 hi = ds_read_tr16(tile + tr_base + (k0 + 8) * P + x0);
+  const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+  const u32x4 r = {l2.x, l2.y, h2.x, h2.y};
+  return as_bf16x8(r);
 }
 
 }  // namespace sppo

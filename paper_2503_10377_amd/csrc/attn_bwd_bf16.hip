@@ -13,6 +13,8 @@
 //   bwd_dq    one workgroup per 128 query rows of one head (lane <-> query);
 //             streams K/V tiles and accumulates dQ^T += K^T dS^T.
 // P = exp2(S*scale*log2e - LSE*log2e), dS = P (dP - Delta).
+#include <type_traits>
+
 #include "sppo_kernels.h"
 #include "tile_common.h"
 
@@ -222,15 +224,11 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   // Query tiles (chunk-local) that can see a key of this workgroup.
   const int64_t qt_begin = k0 > c0 ? (k0 - c0) / BQ : 0;
   const int64_t nqt = (s + BQ - 1) / BQ;
-  const int64_t per_head = nqt - qt_begin;
-  const int64_t total = per_head * G;
 
   const int64_t qstride = (int64_t)a.Hq * D;
   Block4x8 qreg[IPT], dreg[IPT];
   float lse_r = INFINITY, dl_r = 0.f;
-  auto load_tile = [&](int64_t n) {
-    const int h = hk * G + (int)(n / per_head);
-    const int64_t qt = qt_begin + n % per_head;
+  auto load_tile = [&](int h, int64_t qt) {
     const uint16_t* qbase = static_cast<const uint16_t*>(a.q) + (b * s * a.Hq + h) * D;
     const uint16_t* dbase = static_cast<const uint16_t*>(a.dout) + (b * s * a.Hq + h) * D;
 #pragma unroll
@@ -244,47 +242,47 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
     }
     if (tid < BQ) {
       const int64_t rr = qt * BQ + tid;
-      if (rr < s) {
-        lse_r = a.lse[(b * a.Hq + h) * s + rr] * kLog2e;
-        dl_r = a.delta[(b * a.Hq + h) * s + rr];
-      } else {
-        lse_r = INFINITY;
-        dl_r = 0.f;
-      }
+      lse_r = rr < s ? a.lse[(b * a.Hq + h) * s + rr] * kLog2e : INFINITY;
+      dl_r = rr < s ? a.delta[(b * a.Hq + h) * s + rr] : 0.f;
     }
   };
 
-  if (total > 0) load_tile(0);
-  for (int64_t n = 0; n < total; ++n) {
-    const int64_t q0 = c0 + (qt_begin + n % per_head) * BQ;
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < IPT; ++u) {
-      const int c = tid + 256 * u;
-      if (ITEMS % 256 == 0 || c < ITEMS) {
-        const int rg = c / CG, cg = c % CG;
-        store_block_tile<D>(qreg[u], Qs, rg, cg);
-        store_block_tile<D>(dreg[u], Ds, rg, cg);
-      }
-    }
-    if (tid < BQ) {
-      lse2s[tid] = lse_r;
-      dls[tid] = dl_r;
-    }
-    __syncthreads();
-    if (n + 1 < total) load_tile(n + 1);
+  // One query tile, as five scheduling regions (sched_barrier between them
+  // keeps the compiler from sinking LDS reads next to their MFMAs):
+  //   1: natural reads of Q/dO rows 0..31
+  //   2: S, dP MFMAs of rows 0..31        + natural reads of rows 32..63
+  //   3: S, dP MFMAs of rows 32..63       + P, dS of rows 0..31 (VALU)
+  //                                       + transposed Q/dO reads for rows 0..31
+  //   4: dV, dK MFMAs of rows 0..31       + P, dS of rows 32..63
+  //   5: transposed reads for rows 32..63, then their dV, dK MFMAs
+  // so every MFMA batch has its operands in flight one region ahead and the
+  // softmax VALU work of one row block can overlap the MFMAs of the other.
+  // MASK selects the diagonal variant.
+  auto tile_body = [&](int64_t q0, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    const int rel = (int)(j - q0);  // this lane's key relative to the query tile
+    f32x16 sv[2], dp[2];
+    bf16x8 pb[2][2], dsb[2][2];
+    bf16x8 nq[NK], nd[NK];
+    bf16x8 tq[2][ND], td[2][ND];
 
-#pragma unroll
-    for (int ib = 0; ib < BQ / 32; ++ib) {
-      // S[query][key] = Q K^T and dP = dO V^T; lane <-> key.
-      f32x16 sv = f32x16{}, dp = f32x16{};
+    auto nat_reads = [&](int ib) {
 #pragma unroll
       for (int kk = 0; kk < NK; ++kk) {
-        sv = mfma32(ld_lds_nat<D>(Qs, nat, 32 * ib, kk), kf[kk], sv);
-        dp = mfma32(ld_lds_nat<D>(Ds, nat, 32 * ib, kk), vf[kk], dp);
+        nq[kk] = ld_lds_nat<D>(Qs, nat, 32 * ib, kk);
+        nd[kk] = ld_lds_nat<D>(Ds, nat, 32 * ib, kk);
       }
-      const bool need_mask = k0 + 32 * w + 31 > q0 + 32 * ib;
-      const int rel = (int)(j - q0);  // this lane's key relative to the query tile
+    };
+    auto sdp_mfma = [&](int ib) {
+      sv[ib] = f32x16{};
+      dp[ib] = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        sv[ib] = mfma32(nq[kk], kf[kk], sv[ib]);
+        dp[ib] = mfma32(nd[kk], vf[kk], dp[ib]);
+      }
+    };
+    auto softmax = [&](int ib) {
       float p[16], ds[16];
 #pragma unroll
       for (int v4 = 0; v4 < 4; ++v4) {
@@ -296,26 +294,88 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int v = 4 * v4 + e;
-          float pv = fast_exp2(sv[v] * C - lv[e]);
-          if (need_mask && rel > qi + e) pv = 0.f;
+          float pv = fast_exp2(sv[ib][v] * C - lv[e]);
+          if (MASK && rel > qi + e) pv = 0.f;
           p[v] = pv;
-          ds[v] = pv * (dp[v] - dv4[e]);
+          ds[v] = pv * (dp[ib][v] - dv4[e]);
         }
       }
-      bf16x8 pb[2], dsb[2];
-      pb[0] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
-      pb[1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
-      dsb[0] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
-      dsb[1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
-      // dV[key][d] += P^T dO,  dK[key][d] += dS^T Q   (lane <-> d in C).
+      pb[ib][0] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+      pb[ib][1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
+      dsb[ib][0] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
+      dsb[ib][1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
+    };
+    auto tr_reads = [&](int ib, int hh) {
 #pragma unroll
       for (int db = 0; db < ND; ++db) {
+        tq[hh][db] = ld_lds_tr<D>(Qs, trb, 16 * (2 * ib + hh), 32 * db);
+        td[hh][db] = ld_lds_tr<D>(Ds, trb, 16 * (2 * ib + hh), 32 * db);
+      }
+    };
+    auto dkdv_mfma = [&](int ib) {
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int kb = 2 * ib + hh;
-          dv[db] = mfma32(pb[hh], ld_lds_tr<D>(Ds, trb, 16 * kb, 32 * db), dv[db]);
-          dk[db] = mfma32(dsb[hh], ld_lds_tr<D>(Qs, trb, 16 * kb, 32 * db), dk[db]);
+      for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+        for (int db = 0; db < ND; ++db) {
+          dv[db] = mfma32(pb[ib][hh], td[hh][db], dv[db]);
+          dk[db] = mfma32(dsb[ib][hh], tq[hh][db], dk[db]);
         }
+      }
+    };
+
+    nat_reads(0);
+    __builtin_amdgcn_sched_barrier(0);
+    sdp_mfma(0);
+    nat_reads(1);
+    __builtin_amdgcn_sched_barrier(0);
+    sdp_mfma(1);
+    softmax(0);
+    tr_reads(0, 0);
+    tr_reads(0, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    dkdv_mfma(0);
+    softmax(1);
+    __builtin_amdgcn_sched_barrier(0);
+    tr_reads(1, 0);
+    tr_reads(1, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    dkdv_mfma(1);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  load_tile(hk * G, qt_begin);
+  for (int hh = 0; hh < G; ++hh) {
+    for (int64_t qt = qt_begin; qt < nqt; ++qt) {
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < IPT; ++u) {
+        const int c = tid + 256 * u;
+        if (ITEMS % 256 == 0 || c < ITEMS) {
+          const int rg = c / CG, cg = c % CG;
+          store_block_tile<D>(qreg[u], Qs, rg, cg);
+          store_block_tile<D>(dreg[u], Ds, rg, cg);
+        }
+      }
+      if (tid < BQ) {
+        lse2s[tid] = lse_r;
+        dls[tid] = dl_r;
+      }
+      __syncthreads();
+      // Prefetch the next tile (the same one again after the last, harmless).
+      {
+        int nh = hh;
+        int64_t nq = qt + 1;
+        if (nq == nqt) {
+          nq = qt_begin;
+          nh = hh + 1 < G ? hh + 1 : hh;
+        }
+        load_tile(hk * G + nh, nq);
+      }
+      const int64_t q0 = c0 + qt * BQ;
+      if (k0 + 32 * w + 31 > q0) {
+        tile_body(q0, std::true_type{});
+      } else {
+        tile_body(q0, std::false_type{});
       }
     }
   }

@@ -120,6 +120,82 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
     }
   };
 
+  // One K/V tile as scheduling regions (see the dK/dV kernel):
+  //   1: natural K/V reads of keys 0..31
+  //   2: S^T, dP^T MFMAs of keys 0..31  + natural reads of keys 32..63
+  //   3: S^T, dP^T MFMAs of keys 32..63 + P, dS of keys 0..31 (VALU)
+  //                                     + transposed K reads for keys 0..31
+  //   4: dQ MFMAs over keys 0..31       + P, dS of keys 32..63
+  //   5: transposed K reads for keys 32..63, then their dQ MFMAs
+  auto tile_body = [&](int64_t k0, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    const int rel = (int)(r - k0);
+    f32x16 sv[2], dp[2];
+    bf16x8 dsb[4];
+    bf16x8 nk[NK], nv[NK];
+    bf16x8 tk[2][ND];
+
+    auto nat_reads = [&](int jb) {
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        nk[kk] = ld_lds_nat<D>(Ks, nat, 32 * jb, kk);
+        nv[kk] = ld_lds_nat<D>(Vs, nat, 32 * jb, kk);
+      }
+    };
+    auto sdp_mfma = [&](int jb) {
+      sv[jb] = f32x16{};
+      dp[jb] = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        sv[jb] = mfma32(nk[kk], qf[kk], sv[jb]);
+        dp[jb] = mfma32(nv[kk], df[kk], dp[jb]);
+      }
+    };
+    auto softmax = [&](int jb) {
+      float ds[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float p = fast_exp2(sv[jb][v] * C - lse2);
+        if (MASK && 32 * jb + 8 * (v / 4) + 4 * g + (v % 4) > rel) p = 0.f;
+        ds[v] = p * (dp[jb][v] - dl);
+      }
+      dsb[2 * jb] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
+      dsb[2 * jb + 1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
+    };
+    auto tr_reads = [&](int jb) {
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+        for (int db = 0; db < ND; ++db) tk[hh][db] = ld_lds_tr<D>(Ks, trb, 16 * (2 * jb + hh), 32 * db);
+      }
+    };
+    // dQ^T[d][query] += K^T dS^T: K^T comes from transposed reads of K.
+    auto dq_mfma = [&](int jb) {
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+        for (int db = 0; db < ND; ++db) dq[db] = mfma32(tk[hh][db], dsb[2 * jb + hh], dq[db]);
+      }
+    };
+
+    nat_reads(0);
+    __builtin_amdgcn_sched_barrier(0);
+    sdp_mfma(0);
+    nat_reads(1);
+    __builtin_amdgcn_sched_barrier(0);
+    sdp_mfma(1);
+    softmax(0);
+    tr_reads(0);
+    __builtin_amdgcn_sched_barrier(0);
+    dq_mfma(0);
+    softmax(1);
+    __builtin_amdgcn_sched_barrier(0);
+    tr_reads(1);
+    __builtin_amdgcn_sched_barrier(0);
+    dq_mfma(1);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
   load_tile(0);
   for (int it = 0; it < nkv; ++it) {
     const int64_t k0 = (int64_t)it * BC;
@@ -134,36 +210,12 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
       }
     }
     __syncthreads();
-    if (it + 1 < nkv) load_tile(it + 1);
+    load_tile(it + 1 < nkv ? it + 1 : it);  // the last prefetch repeats a tile, harmlessly
 
-    const bool need_mask = k0 + BC - 1 > q0 + 32 * w;
-    const int rel = (int)(r - k0);
-    bf16x8 dsb[4];
-#pragma unroll
-    for (int jb = 0; jb < 2; ++jb) {
-      f32x16 sv = f32x16{}, dp = f32x16{};
-#pragma unroll
-      for (int kk = 0; kk < NK; ++kk) {
-        sv = mfma32(ld_lds_nat<D>(Ks, nat, 32 * jb, kk), qf[kk], sv);
-        dp = mfma32(ld_lds_nat<D>(Vs, nat, 32 * jb, kk), df[kk], dp);
-      }
-      float ds[16];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float p = fast_exp2(sv[v] * C - lse2);
-        if (need_mask && 32 * jb + 8 * (v / 4) + 4 * g + (v % 4) > rel) p = 0.f;
-        ds[v] = p * (dp[v] - dl);
-      }
-      dsb[2 * jb] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
-      dsb[2 * jb + 1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
-    }
-    // dQ^T[d][query] += K^T dS^T: K^T comes from transposed reads of K.
-#pragma unroll
-    for (int db = 0; db < ND; ++db) {
-#pragma unroll
-      for (int kb = 0; kb < BC / 16; ++kb) {
-        dq[db] = mfma32(ld_lds_tr<D>(Ks, trb, 16 * kb, 32 * db), dsb[kb], dq[db]);
-      }
+    if (k0 + BC - 1 > q0 + 32 * w) {
+      tile_body(k0, std::true_type{});
+    } else {
+      tile_body(k0, std::false_type{});
     }
   }
 

@@ -30,6 +30,7 @@ import os
 import sys
 import time
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
 PEAK_BF16_TFLOPS = 256 * 2.4e9 * 4096 / 1e12  # dense bf16 MFMA, MI355X
 HBM_PEAK_GBS = 8000.0
 METRIC = "chunked causal attn fwd+bwd TFLOP/s (% bf16 MFMA peak) + % offload hidden"
@@ -60,30 +61,70 @@ def algorithmic_flops(offsets, B, Hq, D):
     return {"fwd": 4 * p, "bwd_dkdv": 8 * p, "bwd_dq": 2 * p, "bwd_pre": 0, "total": 14 * p}
 
 
-def oracle_cpu_baseline(inp, D, sample_tokens):
-    """Time the fp64 oracle (fwd + bwd, unchunked) on head 0 of the first
-    ``sample_tokens`` tokens of the same inputs."""
+def oracle_cpu_baseline(inp, D, sample_tokens, sample_heads):
+    """Time the fp64 oracle (fwd + bwd, unchunked) on the first
+    ``sample_heads`` heads over the first ``sample_tokens`` tokens of the same
+    inputs (heads one after another, as the oracle runs them)."""
     import numpy as np
 
     import oracle
 
-    def host(t, h):
-        return t[:, :sample_tokens, h:h + 1].float().cpu().numpy().astype(np.float64)
+    def host(t):
+        return t[:, :sample_tokens, :sample_heads].float().cpu().numpy().astype(np.float64)
 
-    q, k, v, do = host(inp["q"], 0), host(inp["k"], 0), host(inp["v"], 0), host(inp["do"], 0)
+    q, k, v, do = host(inp["q"]), host(inp["k"]), host(inp["v"]), host(inp["do"])
     try:
         from threadpoolctl import threadpool_info
-        cores = max(i.get("num_threads", 1) for i in threadpool_info()) if threadpool_info() else 1
+        info = threadpool_info()
+        cores = max(i.get("num_threads", 1) for i in info) if info else 1
     except Exception:
         cores = len(os.sched_getaffinity(0))
     t0 = time.perf_counter()
     oracle.attention(q, k, v, do, 1.0 / math.sqrt(D))
     dt = time.perf_counter() - t0
-    flops = 14 * D * sample_tokens * (sample_tokens + 1) / 2
+    flops = 14 * D * sample_heads * sample_tokens * (sample_tokens + 1) / 2
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"fp64 NumPy oracle, unchunked fwd+bwd of head 0 over the first {sample_tokens} "
-                      f"tokens ({flops:.3e} algorithmic flop in {dt:.2f} s)",
+            "sample": f"fp64 NumPy oracle, unchunked fwd+bwd of heads 0..{sample_heads - 1} over the "
+                      f"first {sample_tokens} tokens ({flops:.3e} algorithmic flop in {dt:.2f} s)",
             "seconds": dt}
+
+
+def kernel_source_hash(kernel):
+    """sha256 of the HIP source that defines ``kernel``."""
+    import hashlib
+
+    src = {"fwd": "attn_fwd_bf16.hip", "bwd_dkdv": "attn_bwd_bf16.hip", "bwd_dq": "attn_bwd_bf16.hip",
+           "bwd_pre": "attn_bwd_bf16.hip"}[kernel]
+    path = os.path.join(ROOT, "paper_2503_10377_amd", "csrc", src)
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of ``kernel`` from the committed counter record
+    (profiles/<kernel>_<workload>_traffic.json), or None when the record is
+    missing or the kernel source changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha256") != kernel_source_hash(kernel):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def copy_calibration(nbytes):
+    """A plain device-to-device copy of ``nbytes``, three times: the known
+    traffic against which FETCH_SIZE / WRITE_SIZE are scaled."""
+    import torch
+
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "copies": 3}), flush=True)
 
 
 def main():
@@ -93,10 +134,16 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
     ap.add_argument("--lookahead", type=int, default=2)
-    ap.add_argument("--cpu-sample-tokens", type=int, default=16384)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=32768)
+    ap.add_argument("--cpu-sample-heads", type=int, default=2)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a device copy of BYTES (counter calibration) and exit")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-offload-compare", action="store_true")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the sharded path is "
               "described, not built.", file=sys.stderr)
@@ -169,7 +216,8 @@ def main():
     dom = max((n for n in kern if flops.get(n)), key=lambda n: kern[n]["ms_per_step"])
     ach = kern[dom]["tflops"]
     res["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
-                       "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": None}
+                       "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS,
+                       "traffic": measured_traffic(dom, args.workload)}
     if cs is not None:
         copy_ms = (cs["ms_d2h"] + cs["ms_h2d"]) / steps
         off = {"bytes_d2h_per_step": cs["bytes_d2h"] / steps, "bytes_h2d_per_step": cs["bytes_h2d"] / steps,
@@ -189,7 +237,7 @@ def main():
     ca.close()
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        cb = oracle_cpu_baseline(inp, D, args.cpu_sample_tokens)
+        cb = oracle_cpu_baseline(inp, D, args.cpu_sample_tokens, args.cpu_sample_heads)
         res["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
     print(json.dumps(res), flush=True)
 

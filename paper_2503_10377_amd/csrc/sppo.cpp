@@ -22,7 +22,6 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
-#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -148,13 +147,7 @@ sppo::ChunkArgs make_args(const sppo_ctx* c, int i) {
 // 1 MiB plus a tail row) because the runtime serves those with the SDMA
 // engines, whereas a linear device->host hipMemcpyAsync is served by a blit
 // kernel that must find free compute units next to the attention kernels.
-bool g_d2h_rect = [] {
-  const char* e = getenv("SPPO_D2H_RECT");
-  return !(e && e[0] == '0');
-}();
-
 hipError_t copy_d2h(void* dst, const void* src, size_t n, hipStream_t s) {
-  if (!g_d2h_rect) return hipMemcpyAsync(dst, src, n, hipMemcpyDeviceToHost, s);
   constexpr size_t W = size_t(1) << 20;
   const size_t rows = n / W, tail = n % W;
   hipError_t e = hipSuccess;

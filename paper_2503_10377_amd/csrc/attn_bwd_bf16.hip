@@ -78,7 +78,8 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
   const int64_t kend = (q0 + BR < c1) ? q0 + BR : c1;
   const int nkv = (int)((kend + BC - 1) / BC);
   const float C = a.scale * kLog2e;
-  const int nat = T::nat_base(lane), trb = T::tr_base(lane);
+  const auto nat = T::nat_base(lane);
+  const auto trb = T::tr_base(lane);
 
   bf16x8 qf[NK], df[NK];
   float lse2 = INFINITY, dl = 0.f;
@@ -255,7 +256,8 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   const int64_t k0 = (int64_t)blockIdx.x * kKvBKV;
   const int64_t j = k0 + 32 * w + l32;  // this lane's key
   const float C = a.scale * kLog2e;
-  const int nat = T::nat_base(lane), trb = T::tr_base(lane);
+  const auto nat = T::nat_base(lane);
+  const auto trb = T::tr_base(lane);
 
   bf16x8 kf[NK], vf[NK];
   {

@@ -49,7 +49,8 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(ChunkArgs a) {
   const int64_t kend = (q0 + BR < c1) ? q0 + BR : c1;
   const int nkv = (int)((kend + BC - 1) / BC);
   const float C = a.scale * kLog2e;
-  const int nat = T::nat_base(lane), trb = T::tr_base(lane);
+  const auto nat = T::nat_base(lane);
+  const auto trb = T::tr_base(lane);
 
   bf16x8 qf[NK];
   {

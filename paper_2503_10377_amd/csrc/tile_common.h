@@ -86,33 +86,52 @@ __device__ __forceinline__ void load_block4x8(Block4x8& blk, const uint16_t* bas
 
 // ---------------------------------------------------------------- LDS tiles
 // A bf16 tile [rows][D] in LDS is stored in natural layout (row = key or
-// query, column = head dim) with row pitch D + 16 elements, and the 16-byte
-// chunk index of row r XOR-ed with bit 2 of r.  For D = 128 this makes all
-// three access patterns free of bank conflicts on the 32-bank LDS: the 4x8
-// block stores, the natural MFMA-operand reads (rows l%32, 16-byte chunks),
-// and the ds_read_b64_tr_b16 transposed reads.  Every swizzle term is a
-// per-lane constant, so each access is a lane base plus an immediate.
+// query, column = head dim) with row pitch D + 32 elements, and the 16-byte
+// chunk index c of row r stored at c ^ ((r >> 2) & 3).  The gfx950 LDS has 64
+// four-byte banks; a ds_read_b128 is served 16 lanes at a time, a
+// ds_read_b64 / ds_read_b64_tr_b16 32 lanes at a time, and a ds_write_b128 8
+// lanes at a time.  With this layout every group touches 64 distinct banks
+// (or fewer, disjoint) for the three access patterns used here:
+//   * natural operand reads: 16 consecutive rows, one chunk each -- the
+//     pitch puts rows r and r+1 4 chunks apart (mod 16) and the swizzle
+//     separates r and r+4;
+//   * transposed reads: 4 rows x 4 chunks per 32 lanes, each row's 4 chunks
+//     a distinct quarter of the 256-byte bank window;
+//   * 4x8-block stores: 8 chunks of one row.
+// The swizzle only touches the two low bits of the chunk index, so every
+// access is a per-lane base (one per parity of the k-step for natural reads,
+// one per 8-row half for transposed reads) plus an immediate offset.
 template <int D>
 struct LdsTile {
-  static constexpr int P = D + 16;
+  static constexpr int P = D + 32;
   static constexpr int CG = D / 8;  // 16-byte chunks per row
+  static __device__ __forceinline__ int swz(int row) { return (row >> 2) & 3; }
   // Element offset of row 4*rg + x, 16-byte chunk cg.
   static __device__ __forceinline__ int store_off(int rg, int x, int cg) {
-    return (4 * rg + x) * P + 8 * (cg ^ (rg & 1));
+    return (4 * rg + x) * P + 8 * (cg ^ (rg & 3));
   }
-  // Lane base of a natural operand read: row l%32, chunk 2*kk + l/32 (add
-  // rb*P + 16*kk for row block rb, rb % 32 == 0, and k-step kk).
-  static __device__ __forceinline__ int nat_base(int lane) {
-    const int l32 = lane & 31, g = lane >> 5;
-    return l32 * P + 8 * (g ^ ((l32 >> 2) & 1));
+  // Lane bases of natural operand reads: row l%32, chunk 2*kk + l/32, for
+  // even and odd k-steps kk (add rb*P + 32*(kk/2) for row block rb, rb % 32
+  // == 0).
+  struct Nat {
+    int b[2];
+  };
+  static __device__ __forceinline__ Nat nat_base(int lane) {
+    const int l32 = lane & 31, g = lane >> 5, s = swz(l32);
+    return Nat{{l32 * P + 8 * (g ^ s), l32 * P + 8 * ((2 + g) ^ s)}};
   }
-  // Lane base of a transposed read (add (k0 + {0,8})*P + x0 with k0 % 16 == 0
-  // and x0 % 32 == 0).  Source lane s = 16q + 4e + a supplies the 8 bytes at
-  // row 4*(q/2) + e, column 16*(q%2) + 4*a; ds_read_b64_tr_b16 hands output
-  // lane 16q + 4a' + b element b of source lanes 16q + 4e + a', e = 0..3.
-  static __device__ __forceinline__ int tr_base(int lane) {
+  // Lane bases of a transposed read of rows k0..k0+7 (b[0]) and
+  // k0+8..k0+15 (b[1]); add k0*P (+8*P for b[1]) + x0 with k0 % 16 == 0 and
+  // x0 % 32 == 0.  Source lane s = 16q + 4e + a supplies the 8 bytes at row
+  // 4*(q/2) + e, column 16*(q%2) + 4*a; ds_read_b64_tr_b16 hands output lane
+  // 16q + 4a' + b element b of source lanes 16q + 4e + a', e = 0..3.
+  struct Tr {
+    int b[2];
+  };
+  static __device__ __forceinline__ Tr tr_base(int lane) {
     const int q = lane >> 4, e = (lane >> 2) & 3, a = lane & 3;
-    return (4 * (q >> 1) + e) * P + 8 * ((2 * (q & 1) + (a >> 1)) ^ ((q >> 1) & 1)) + 4 * (a & 1);
+    const int row = 4 * (q >> 1) + e, c = 2 * (q & 1) + (a >> 1);
+    return Tr{{row * P + 8 * (c ^ (q >> 1)) + 4 * (a & 1), row * P + 8 * (c ^ ((q >> 1) + 2)) + 4 * (a & 1)}};
   }
 };
 
@@ -126,8 +145,9 @@ __device__ __forceinline__ void store_block_tile(const Block4x8& blk, uint16_t* 
 
 // Natural operand: lane l gets row rb + l%32, columns 16*kk + 8*(l/32) + 0..7.
 template <int D>
-__device__ __forceinline__ bf16x8 ld_lds_nat(const uint16_t* tile, int nat_base, int rb, int kk) {
-  return as_bf16x8(*reinterpret_cast<const u32x4*>(tile + nat_base + rb * LdsTile<D>::P + 16 * kk));
+__device__ __forceinline__ bf16x8 ld_lds_nat(const uint16_t* tile, const typename LdsTile<D>::Nat& nat, int rb,
+                                             int kk) {
+  return as_bf16x8(*reinterpret_cast<const u32x4*>(tile + nat.b[kk & 1] + rb * LdsTile<D>::P + 32 * (kk >> 1)));
 }
 
 __device__ __forceinline__ v4i16 ds_read_tr16(const uint16_t* p) {
@@ -138,10 +158,10 @@ __device__ __forceinline__ v4i16 ds_read_tr16(const uint16_t* p) {
 // rows k0 + {8*(e/4) + 4*(l/32) + e%4 : e = 0..7}, i.e. the permuted k-slot
 // map, so it pairs with an operand taken from C-tile registers.
 template <int D>
-__device__ __forceinline__ bf16x8 ld_lds_tr(const uint16_t* tile, int tr_base, int k0, int x0) {
+__device__ __forceinline__ bf16x8 ld_lds_tr(const uint16_t* tile, const typename LdsTile<D>::Tr& tr, int k0, int x0) {
   constexpr int P = LdsTile<D>::P;
-  const v4i16 lo = ds_read_tr16(tile + tr_base + k0 * P + x0);
-  const v4i16 hi = ds_read_tr16(tile + tr_base + (k0 + 8) * P + x0);
+  const v4i16 lo = ds_read_tr16(tile + tr.b[0] + k0 * P + x0);
+  const v4i16 hi = ds_read_tr16(tile + tr.b[1] + (k0 + 8) * P + x0);
   const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
   const u32x4 r = {l2.x, l2.y, h2.x, h2.y};
   return as_bf16x8(r);

@@ -108,15 +108,21 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
   for (int db = 0; db < ND; ++db) dq[db] = f32x16{};
 
   Block4x8 kreg[IPT], vreg[IPT];
+  Block4x8Offsets boff[IPT];
+#pragma unroll
+  for (int u = 0; u < IPT; ++u) {
+    const int c = tid + 256 * u;
+    boff[u] = block4x8_offsets(c / CG, c % CG, kvstride);
+  }
   auto load_tile = [&](int it) {
     const int64_t k0 = (int64_t)it * BC;
+    const auto rk = tile_rsrc(kbase + k0 * kvstride, c1 - k0, BC, kvstride);
+    const auto rv = tile_rsrc(vbase + k0 * kvstride, c1 - k0, BC, kvstride);
 #pragma unroll
     for (int u = 0; u < IPT; ++u) {
-      const int c = tid + 256 * u;
-      if (ITEMS % 256 == 0 || c < ITEMS) {
-        const int rg = c / CG, cg = c % CG;
-        load_block4x8(kreg[u], kbase, kvstride, k0 + 4 * rg, c1, 8 * cg);
-        load_block4x8(vreg[u], vbase, kvstride, k0 + 4 * rg, c1, 8 * cg);
+      if (ITEMS % 256 == 0 || tid + 256 * u < ITEMS) {
+        load_block4x8(kreg[u], rk, boff[u]);
+        load_block4x8(vreg[u], rv, boff[u]);
       }
     }
   };
@@ -281,17 +287,22 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
 
   const int64_t qstride = (int64_t)a.Hq * D;
   Block4x8 qreg[IPT], dreg[IPT];
+  Block4x8Offsets boff[IPT];
+#pragma unroll
+  for (int u = 0; u < IPT; ++u) {
+    const int c = tid + 256 * u;
+    boff[u] = block4x8_offsets(c / CG, c % CG, qstride);
+  }
   float lse_r = INFINITY, dl_r = 0.f;
   auto load_tile = [&](int h, int64_t qt) {
-    const uint16_t* qbase = static_cast<const uint16_t*>(a.q) + (b * s * a.Hq + h) * D;
-    const uint16_t* dbase = static_cast<const uint16_t*>(a.dout) + (b * s * a.Hq + h) * D;
+    const int64_t tile0 = (b * s + qt * BQ) * a.Hq + h;  // first row of the tile, in D-element units
+    const auto rq = tile_rsrc(static_cast<const uint16_t*>(a.q) + tile0 * D, s - qt * BQ, BQ, qstride);
+    const auto rd = tile_rsrc(static_cast<const uint16_t*>(a.dout) + tile0 * D, s - qt * BQ, BQ, qstride);
 #pragma unroll
     for (int u = 0; u < IPT; ++u) {
-      const int c = tid + 256 * u;
-      if (ITEMS % 256 == 0 || c < ITEMS) {
-        const int rg = c / CG, cg = c % CG;
-        load_block4x8(qreg[u], qbase, qstride, qt * BQ + 4 * rg, s, 8 * cg);
-        load_block4x8(dreg[u], dbase, qstride, qt * BQ + 4 * rg, s, 8 * cg);
+      if (ITEMS % 256 == 0 || tid + 256 * u < ITEMS) {
+        load_block4x8(qreg[u], rq, boff[u]);
+        load_block4x8(dreg[u], rd, boff[u]);
       }
     }
     if (tid < BQ) {

@@ -71,15 +71,21 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(ChunkArgs a) {
   float m = -INFINITY, lsum = 0.f;
 
   Block4x8 kreg[IPT], vreg[IPT];
+  Block4x8Offsets boff[IPT];
+#pragma unroll
+  for (int u = 0; u < IPT; ++u) {
+    const int c = tid + 256 * u;
+    boff[u] = block4x8_offsets(c / CG, c % CG, kvstride);
+  }
   auto load_tile = [&](int it) {
     const int64_t k0 = (int64_t)it * BC;
+    const auto rk = tile_rsrc(kbase + k0 * kvstride, c1 - k0, BC, kvstride);
+    const auto rv = tile_rsrc(vbase + k0 * kvstride, c1 - k0, BC, kvstride);
 #pragma unroll
     for (int u = 0; u < IPT; ++u) {
-      const int c = tid + 256 * u;
-      if (ITEMS % 256 == 0 || c < ITEMS) {
-        const int rg = c / CG, cg = c % CG;
-        load_block4x8(kreg[u], kbase, kvstride, k0 + 4 * rg, c1, 8 * cg);
-        load_block4x8(vreg[u], vbase, kvstride, k0 + 4 * rg, c1, 8 * cg);
+      if (ITEMS % 256 == 0 || tid + 256 * u < ITEMS) {
+        load_block4x8(kreg[u], rk, boff[u]);
+        load_block4x8(vreg[u], rv, boff[u]);
       }
     }
   };

@@ -68,20 +68,36 @@ struct Block4x8 {
   u32x4 r[4];
 };
 
-// Rows [row0, row0+4) x cols [col0, col0+8) of a row-major bf16 matrix
-// whose row x starts at base + x*row_stride; rows >= row_limit read as 0.
-__device__ __forceinline__ void load_block4x8(Block4x8& blk, const uint16_t* base, int64_t row_stride,
-                                              int64_t row0, int64_t row_limit, int col0) {
-  const uint16_t* p = base + row0 * row_stride + col0;
-  if (row0 + 4 <= row_limit) {
+// Blocks are loaded through a buffer resource based at the first row of a
+// tile: the hardware range check returns zero for every byte offset at or
+// past num_records, so rows >= valid_rows read as zero with no per-lane test,
+// and the per-lane byte offsets stay the same from tile to tile (only the
+// scalar base moves).  Offsets are relative to the tile base, so they fit in
+// 32 bits whatever the tensor size.
+constexpr int kBufferFlags = 0x00020000;  // dword 3 of a raw gfx9 buffer resource
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* tile_base, int64_t valid_rows,
+                                                            int tile_rows, int64_t row_stride) {
+  const int64_t n = valid_rows <= 0 ? 0 : (valid_rows < tile_rows ? valid_rows : tile_rows);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(tile_base), (short)0,
+                                           (int)(n * row_stride * (int64_t)sizeof(uint16_t)), kBufferFlags);
+}
+
+// Byte offsets of rows 4*rg + x, columns 8*cg.. of a tile with the given row
+// stride (elements).
+struct Block4x8Offsets {
+  int b[4];
+};
+__device__ __forceinline__ Block4x8Offsets block4x8_offsets(int rg, int cg, int64_t row_stride) {
+  Block4x8Offsets o;
 #pragma unroll
-    for (int x = 0; x < 4; ++x) blk.r[x] = ld_global16(p + x * row_stride);
-  } else {
+  for (int x = 0; x < 4; ++x) o.b[x] = (int)(((4 * rg + x) * row_stride + 8 * cg) * (int64_t)sizeof(uint16_t));
+  return o;
+}
+
+__device__ __forceinline__ void load_block4x8(Block4x8& blk, __amdgpu_buffer_rsrc_t rsrc, const Block4x8Offsets& off) {
 #pragma unroll
-    for (int x = 0; x < 4; ++x) {
-      blk.r[x] = (row0 + x < row_limit) ? ld_global16(p + x * row_stride) : u32x4{0u, 0u, 0u, 0u};
-    }
-  }
+  for (int x = 0; x < 4; ++x) blk.r[x] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off.b[x], 0, 0);
 }
 
 // ---------------------------------------------------------------- LDS tiles

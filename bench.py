@@ -15,7 +15,8 @@ Reported (one JSON line):
                  flop/clk/CU, dense)
   offload_hidden 1 - max(0, T_on - T_off) / T_copy, where T_off is the same
                  step without offload and T_copy the event-timed copy busy
-                 time per step
+                 time per step; the same for the K/V-evicting walk under
+                 offload.evict
   roofline       the dominant kernel (largest summed time), from HIP events
                  around every launch on the compute stream in K further timed
                  steps (kept out of the headline steps)
@@ -240,6 +241,18 @@ def main():
             off["ms_per_step_no_offload"] = ms_off
             off["exposed_ms_per_step"] = exposed
             off["hidden_pct"] = 100.0 * max(0.0, min(1.0, 1.0 - exposed / copy_ms)) if copy_ms > 0 else None
+            if offload == "qkvol":
+                # The same walk with the K/V cache rows given up after the
+                # forward and streamed back under the last chunk's backward.
+                ca_ev = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="qkvol_evict")
+                ms_evict, _, cs_ev = timed(ca_ev, steps, False)
+                ca_ev.close()
+                copy_ev = (cs_ev["ms_d2h"] + cs_ev["ms_h2d"]) / steps
+                exp_ev = max(0.0, ms_evict - ms_off)
+                off["evict"] = {
+                    "ms_per_step": ms_evict, "bytes_h2d_per_step": cs_ev["bytes_h2d"] / steps,
+                    "copy_ms_per_step": copy_ev, "exposed_ms_per_step": exp_ev,
+                    "hidden_pct": 100.0 * max(0.0, min(1.0, 1.0 - exp_ev / copy_ev)) if copy_ev > 0 else None}
         res["offload"] = off
         res["offload_hidden_pct"] = off.get("hidden_pct")
     ca.close()

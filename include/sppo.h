@@ -64,13 +64,24 @@ typedef enum {
 typedef enum { SPPO_F32 = 0, SPPO_BF16 = 1 } sppo_dtype;
 
 /* Which saved activations of a chunk travel to host memory after its
- * forward (two-level activation management, Sec. 5.1).  K/V always stay
- * resident on the device as the skeletal level. */
+ * forward (two-level activation management, Sec. 5.1).  In the first three
+ * modes K/V stay resident on the device as the skeletal level. */
 typedef enum {
   SPPO_OFFLOAD_NONE = 0,  /* nothing leaves the device                      */
   SPPO_OFFLOAD_QOL = 1,   /* Q_i, O_i, LSE_i offloaded and prefetched back  */
-  SPPO_OFFLOAD_QKVOL = 2  /* as QOL, plus a host copy of K_i and V_i; the
+  SPPO_OFFLOAD_QKVOL = 2, /* as QOL, plus a host copy of K_i and V_i; the
                              resident K/V cache is not re-fetched           */
+  SPPO_OFFLOAD_QKVOL_EVICT = 3
+                          /* as QKVOL, but once the forward walk is over the
+                             K/V cache rows of offloaded chunks count as
+                             evicted (the caller may reuse that memory
+                             after sppo_offload_wait): they come back with
+                             sppo_prefetch_kv, and the backward of the last
+                             chunk, the only one that runs before all of
+                             them are back, does its dK/dV work one KV
+                             chunk at a time, each piece waiting only for
+                             its own rows, so the K/V copies stream in
+                             under it                                      */
 } sppo_offload;
 
 /* The problem, in the paper's notation (B, S, N, s_i) plus the attention
@@ -151,7 +162,10 @@ sppo_status sppo_attn_fwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i,
  * so the accumulators need no zeroing; rows >= c_{i+1} are never touched.
  * Calls must come in order i = N-1..0 after fwd(N-1).  If chunk i was
  * offloaded, the stream first waits for the prefetch of chunk i, which must
- * have been issued (otherwise STATE). */
+ * have been issued (otherwise STATE).  With QKVOL_EVICT, bwd(N-1) requires
+ * sppo_prefetch_kv of every offloaded chunk (otherwise STATE) and runs its
+ * dK/dV kernel once per KV chunk j = N-1..0, each launch after chunk j's
+ * K/V-ready event, then dQ. */
 sppo_status sppo_attn_bwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i,
                                 const void* k, const void* v, const void* o_i,
                                 const float* lse_i, const void* do_i,
@@ -180,6 +194,18 @@ sppo_status sppo_offload_wait(sppo_ctx* ctx, int32_t i, void* stream);
  * Requires the offload of chunk i to have been issued. */
 sppo_status sppo_prefetch(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* dst,
                           void* stream);
+
+/* QKVOL_EVICT only: copy chunk i's K_i/V_i rows from host slot i back into
+ * the device K/V cache (k, v: base pointers of the full [B, S, Hkv, D]
+ * tensors) on the context's H2D stream, after everything already enqueued
+ * on `stream` and after chunk i's offload has completed, and record chunk
+ * i's K/V-ready event.  Allowed once the forward walk is over (in_bwd) and
+ * before the backward of chunk N-1, which requires it for every offloaded
+ * chunk and waits for chunk j's K/V-ready event right before the dK/dV work
+ * on chunk j's key rows.  Errors: STATE (other mode, forward walk not over,
+ * chunk not offloaded, already prefetched, backward already started),
+ * INVALID_ARG. */
+sppo_status sppo_prefetch_kv(sppo_ctx* ctx, int32_t i, void* k, void* v, void* stream);
 
 /* Abandon the current forward/backward walk (e.g. after a forward-only run):
  * the next call must be fwd(0).  Clears per-chunk offload state. */

@@ -14,7 +14,11 @@ B > 1 the chunk-local tensors are separate contiguous buffers.
 Offload policy (``offload_chunks``): by default every chunk except the last
 is offloaded -- the last chunk's backward runs right after its forward, so
 sending its activations away and back could only add time.  Prefetches run
-``lookahead`` chunks ahead of the backward walk.
+``lookahead`` chunks ahead of the backward walk.  With ``qkvol_evict`` the
+K/V cache rows of the offloaded chunks are given up once the forward walk is
+over; their copies are queued on the host-to-device stream right before the
+backward of the last chunk, whose dK/dV work consumes them chunk by chunk in
+the order they arrive.
 """
 from __future__ import annotations
 
@@ -103,6 +107,20 @@ class ChunkedAttention:
                         qc[i].fill_(float("nan"))
                         oc[i].fill_(float("nan"))
                         lse[i].fill_(float("nan"))
+        if self.offload == L.SPPO_OFFLOAD_QKVOL_EVICT:
+            kv_chunks = sorted(offl, reverse=True)
+            if poison:
+                # Test hook: the evicted K/V rows are dead once their copies
+                # have landed; overwrite them with NaN.
+                for j in kv_chunks:
+                    L.sppo_offload_wait(self.ctx, j, s)
+                with torch.cuda.stream(s):
+                    for j in kv_chunks:
+                        c0, c1 = self.offsets[j], self.offsets[j + 1]
+                        k[:, c0:c1].fill_(float("nan"))
+                        v[:, c0:c1].fill_(float("nan"))
+            for j in kv_chunks:
+                L.sppo_prefetch_kv(self.ctx, j, k, v, s)
         pending = sorted(offl, reverse=True)
         nxt = 0
         for i in reversed(range(self.N)):

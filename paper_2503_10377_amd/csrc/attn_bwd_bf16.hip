@@ -259,7 +259,8 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   const int64_t b = blockIdx.z;
   const int G = a.Hq / a.Hkv;
   const int64_t c0 = a.c0, c1 = a.c1, s = c1 - c0;
-  const int64_t k0 = (int64_t)blockIdx.x * kKvBKV;
+  const int64_t kv1 = a.kv1;
+  const int64_t k0 = a.kv0 + (int64_t)blockIdx.x * kKvBKV;
   const int64_t j = k0 + 32 * w + l32;  // this lane's key
   const float C = a.scale * kLog2e;
   const auto nat = T::nat_base(lane);
@@ -272,8 +273,8 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
     const uint16_t* vrow = static_cast<const uint16_t*>(a.v) + off;
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) {
-      kf[kk] = j < c1 ? as_bf16x8(ld_global16(krow + 16 * kk + 8 * g)) : bf16x8{};
-      vf[kk] = j < c1 ? as_bf16x8(ld_global16(vrow + 16 * kk + 8 * g)) : bf16x8{};
+      kf[kk] = j < kv1 ? as_bf16x8(ld_global16(krow + 16 * kk + 8 * g)) : bf16x8{};
+      vf[kk] = j < kv1 ? as_bf16x8(ld_global16(vrow + 16 * kk + 8 * g)) : bf16x8{};
     }
   }
 
@@ -445,13 +446,13 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
     }
   }
 
-  // Write back rows [k0, k0+128) n [0, c1): lane <-> d, v <-> key.
+  // Write back rows [k0, k0+128) n [kv0, kv1): lane <-> d, v <-> key.
 #pragma unroll
   for (int db = 0; db < ND; ++db) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int64_t key = k0 + 32 * w + 8 * (v / 4) + 4 * g + (v % 4);
-      if (key < c1) {
+      if (key < kv1) {
         const int64_t idx = ((b * a.S + key) * a.Hkv + hk) * D + 32 * db + l32;
         const float kval = dk[db][v] * a.scale;
         const float vval = dv[db][v];
@@ -484,7 +485,8 @@ hipError_t launch_bwd_pre_bf16(const ChunkArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_bwd_dkdv_bf16(const ChunkArgs& a, hipStream_t stream) {
-  dim3 grid((unsigned)((a.c1 + kKvBKV - 1) / kKvBKV), (unsigned)a.Hkv, (unsigned)a.B);
+  if (a.kv0 < 0 || a.kv1 > a.c1 || a.kv0 >= a.kv1) return hipErrorInvalidValue;
+  dim3 grid((unsigned)((a.kv1 - a.kv0 + kKvBKV - 1) / kKvBKV), (unsigned)a.Hkv, (unsigned)a.B);
   if (a.D == 128) {
     hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, grid, dim3(256), 0, stream, a);
   } else if (a.D == 64) {

@@ -149,9 +149,9 @@ __global__ __launch_bounds__(kT) void dkdv_f32_kernel(ChunkArgs a) {
   const int64_t b = blockIdx.z;
   const int G = a.Hq / a.Hkv;
   const int64_t c0 = a.c0, c1 = a.c1, s = c1 - c0;
-  const int64_t k0 = (int64_t)blockIdx.x * kT;
+  const int64_t k0 = a.kv0 + (int64_t)blockIdx.x * kT;
   const int64_t j = k0 + tid;
-  const bool jvalid = j < c1;
+  const bool jvalid = j < a.kv1;
   const int64_t kvoff = ((b * a.S + j) * a.Hkv + hk) * D;
   float kr[D], vr[D], dk[D], dv[D];
   for (int d = 0; d < D; ++d) {
@@ -243,7 +243,8 @@ hipError_t launch_bwd_pre_f32(const ChunkArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_bwd_dkdv_f32(const ChunkArgs& a, hipStream_t stream) {
-  dim3 grid((unsigned)((a.c1 + kT - 1) / kT), (unsigned)a.Hkv, (unsigned)a.B);
+  if (a.kv0 < 0 || a.kv1 > a.c1 || a.kv0 >= a.kv1) return hipErrorInvalidValue;
+  dim3 grid((unsigned)((a.kv1 - a.kv0 + kT - 1) / kT), (unsigned)a.Hkv, (unsigned)a.B);
   if (a.D == 64) {
     hipLaunchKernelGGL(dkdv_f32_kernel<64>, grid, dim3(kT), 0, stream, a);
   } else if (a.D == 128) {

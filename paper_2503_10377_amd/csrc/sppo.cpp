@@ -17,6 +17,11 @@
 //                     waits for E_call[i] and E_off[i], copies Q/O/LSE back
 //                     and records E_pf[i].
 //   bwd_chunk(i)    : the caller stream waits for E_pf[i] before its kernels.
+// With K/V eviction (QKVOL_EVICT) the K/V cache rows of offloaded chunks are
+// dead once the forward walk is over:
+//   prefetch_kv(j)  : like prefetch, for K_j/V_j, recording E_kv[j];
+//   bwd_chunk(N-1)  : dK/dV kernel once per KV chunk j = N-1..0, the launch
+//                     for chunk j after E_kv[j]; dQ after all of them.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -57,9 +62,9 @@ struct sppo_ctx {
   hipStream_t d2h = nullptr, h2d = nullptr;
   float* delta = nullptr;
   std::vector<HostSlot> slots;
-  std::vector<hipEvent_t> ev_fwd, ev_off, ev_call, ev_pf;
-  std::vector<EventPair> t_d2h, t_h2d;
-  std::vector<uint8_t> offloaded, prefetched;
+  std::vector<hipEvent_t> ev_fwd, ev_off, ev_call, ev_pf, ev_kv;
+  std::vector<EventPair> t_d2h, t_h2d, t_h2d_kv;
+  std::vector<uint8_t> offloaded, prefetched, kv_prefetched;
   bool in_bwd = false;
   int next_fwd = 0, next_bwd = -1;
   uint64_t bytes_d2h = 0, bytes_h2d = 0;
@@ -108,7 +113,10 @@ size_t bytes_lse(const sppo_ctx* c, int i) {
 size_t bytes_kv_row_block(const sppo_ctx* c, int i) {  // one batch entry's K_i rows
   return (size_t)chunk_len(c, i) * c->prob.n_kv_heads * c->prob.head_dim * c->elt;
 }
-bool offload_kv(const sppo_ctx* c) { return c->prob.offload == SPPO_OFFLOAD_QKVOL; }
+bool offload_kv(const sppo_ctx* c) {
+  return c->prob.offload == SPPO_OFFLOAD_QKVOL || c->prob.offload == SPPO_OFFLOAD_QKVOL_EVICT;
+}
+bool evict_kv(const sppo_ctx* c) { return c->prob.offload == SPPO_OFFLOAD_QKVOL_EVICT; }
 
 sppo_status check_ctx_index(sppo_ctx* ctx, int32_t i) {
   if (!ctx) return SPPO_ERR_INVALID_ARG;
@@ -140,6 +148,8 @@ sppo::ChunkArgs make_args(const sppo_ctx* c, int i) {
   a.D = c->prob.head_dim;
   a.scale = c->scale;
   a.delta = c->delta;
+  a.kv0 = 0;
+  a.kv1 = a.c1;
   return a;
 }
 
@@ -170,6 +180,8 @@ void fold(EventPair& p, double& total) {
 }
 
 // Launch one kernel, bracketed by timing events when kernel timing is on.
+// `slot` < 2N picks the event pair (chunk i uses slot i; the extra dK/dV
+// launches of an evicting bwd(N-1) use N + j).
 template <class F>
 hipError_t timed_launch(sppo_ctx* c, int kind, int i, hipStream_t s, F&& launch) {
   if (!c->ktiming) return launch();
@@ -187,12 +199,12 @@ hipError_t timed_launch(sppo_ctx* c, int kind, int i, hipStream_t s, F&& launch)
 void destroy_all(sppo_ctx* c) {
   if (c->d2h) (void)hipStreamSynchronize(c->d2h);
   if (c->h2d) (void)hipStreamSynchronize(c->h2d);
-  for (auto* v : {&c->ev_fwd, &c->ev_off, &c->ev_call, &c->ev_pf}) {
+  for (auto* v : {&c->ev_fwd, &c->ev_off, &c->ev_call, &c->ev_pf, &c->ev_kv}) {
     for (hipEvent_t e : *v) {
       if (e) (void)hipEventDestroy(e);
     }
   }
-  for (auto* v : {&c->t_d2h, &c->t_h2d, &c->t_kern[0], &c->t_kern[1], &c->t_kern[2], &c->t_kern[3]}) {
+  for (auto* v : {&c->t_d2h, &c->t_h2d, &c->t_h2d_kv, &c->t_kern[0], &c->t_kern[1], &c->t_kern[2], &c->t_kern[3]}) {
     for (EventPair& p : *v) {
       if (p.start) (void)hipEventDestroy(p.start);
       if (p.stop) (void)hipEventDestroy(p.stop);
@@ -246,7 +258,8 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
   if (p->head_dim != 64 && p->head_dim != 128) {
     return fail(nullptr, SPPO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
   }
-  if (p->offload != SPPO_OFFLOAD_NONE && p->offload != SPPO_OFFLOAD_QOL && p->offload != SPPO_OFFLOAD_QKVOL) {
+  if (p->offload != SPPO_OFFLOAD_NONE && p->offload != SPPO_OFFLOAD_QOL && p->offload != SPPO_OFFLOAD_QKVOL &&
+      p->offload != SPPO_OFFLOAD_QKVOL_EVICT) {
     return fail(nullptr, SPPO_ERR_INVALID_ARG, "unknown offload mode");
   }
   if (!(p->softmax_scale >= 0.f) || std::isinf(p->softmax_scale)) {
@@ -295,7 +308,7 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
     return bail(SPPO_ERR_HIP, std::string("hipStreamCreateWithFlags: ") + hipGetErrorString(e));
   }
   const int N = p->n_chunks;
-  for (auto* v : {&c->ev_fwd, &c->ev_off, &c->ev_call, &c->ev_pf}) {
+  for (auto* v : {&c->ev_fwd, &c->ev_off, &c->ev_call, &c->ev_pf, &c->ev_kv}) {
     v->assign(N, nullptr);
     for (int i = 0; i < N; ++i) {
       if ((e = hipEventCreateWithFlags(&(*v)[i], hipEventDisableTiming)) != hipSuccess) {
@@ -304,7 +317,7 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
       }
     }
   }
-  for (auto* v : {&c->t_d2h, &c->t_h2d}) {
+  for (auto* v : {&c->t_d2h, &c->t_h2d, &c->t_h2d_kv}) {
     v->assign(N, EventPair{});
     for (int i = 0; i < N; ++i) {
       if ((e = hipEventCreate(&(*v)[i].start)) != hipSuccess || (e = hipEventCreate(&(*v)[i].stop)) != hipSuccess) {
@@ -314,6 +327,7 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
   }
   c->offloaded.assign(N, 0);
   c->prefetched.assign(N, 0);
+  c->kv_prefetched.assign(N, 0);
   c->slots.assign(N, HostSlot{});
   if (p->offload != SPPO_OFFLOAD_NONE) {
     for (int i = 0; i < N; ++i) {
@@ -382,6 +396,7 @@ sppo_status sppo_attn_fwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i, const
   if (i == 0) {
     std::fill(ctx->offloaded.begin(), ctx->offloaded.end(), 0);
     std::fill(ctx->prefetched.begin(), ctx->prefetched.end(), 0);
+    std::fill(ctx->kv_prefetched.begin(), ctx->kv_prefetched.end(), 0);
   }
   if (++ctx->next_fwd == ctx->prob.n_chunks) {
     ctx->in_bwd = true;
@@ -408,6 +423,15 @@ sppo_status sppo_attn_bwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i, const
   if (ctx->offloaded[i] && !ctx->prefetched[i]) {
     return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " was offloaded but not prefetched");
   }
+  const int N = ctx->prob.n_chunks;
+  const bool pieces = evict_kv(ctx) && i == N - 1;
+  if (pieces) {
+    for (int j = 0; j < N; ++j) {
+      if (ctx->offloaded[j] && !ctx->kv_prefetched[j]) {
+        return fail(ctx, SPPO_ERR_STATE, "K/V of chunk " + std::to_string(j) + " evicted and not prefetched");
+      }
+    }
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (ctx->prefetched[i]) SPPO_HIP(ctx, hipStreamWaitEvent(s, ctx->ev_pf[i], 0));
   sppo::ChunkArgs a = make_args(ctx, i);
@@ -425,9 +449,21 @@ sppo_status sppo_attn_bwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i, const
   hipError_t e = timed_launch(ctx, SPPO_KERNEL_BWD_PRE, i, s, [&] {
     return bf16 ? sppo::launch_bwd_pre_bf16(a, s) : sppo::launch_bwd_pre_f32(a, s);
   });
-  if (e == hipSuccess) {
+  if (e == hipSuccess && !pieces) {
     e = timed_launch(ctx, SPPO_KERNEL_BWD_DKDV, i, s, [&] {
       return bf16 ? sppo::launch_bwd_dkdv_bf16(a, s) : sppo::launch_bwd_dkdv_f32(a, s);
+    });
+  }
+  // Evicting bwd(N-1): key rows of chunk j only once chunk j's K/V are back;
+  // the pieces cover [0, c_N) disjointly, so overwriting is still right.
+  for (int j = N - 1; pieces && j >= 0 && e == hipSuccess; --j) {
+    if (ctx->kv_prefetched[j]) e = hipStreamWaitEvent(s, ctx->ev_kv[j], 0);
+    if (e != hipSuccess) break;
+    sppo::ChunkArgs aj = a;
+    aj.kv0 = ctx->off[j];
+    aj.kv1 = ctx->off[j + 1];
+    e = timed_launch(ctx, SPPO_KERNEL_BWD_DKDV, j == N - 1 ? j : N + j, s, [&] {
+      return bf16 ? sppo::launch_bwd_dkdv_bf16(aj, s) : sppo::launch_bwd_dkdv_f32(aj, s);
     });
   }
   if (e == hipSuccess) {
@@ -531,6 +567,44 @@ sppo_status sppo_prefetch(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* dst, 
   return SPPO_OK;
 }
 
+sppo_status sppo_prefetch_kv(sppo_ctx* ctx, int32_t i, void* k, void* v, void* stream) {
+  sppo_status st = check_ctx_index(ctx, i);
+  if (st != SPPO_OK) return st;
+  if (!evict_kv(ctx)) return fail(ctx, SPPO_ERR_STATE, "K/V prefetch needs a context created with QKVOL_EVICT");
+  if ((st = check_ptr(ctx, k, "k")) || (st = check_ptr(ctx, v, "v"))) return st;
+  if (!ctx->in_bwd) return fail(ctx, SPPO_ERR_STATE, "K/V prefetch before the forward walk is over");
+  if (ctx->next_bwd != ctx->prob.n_chunks - 1) {
+    return fail(ctx, SPPO_ERR_STATE, "K/V prefetch after the backward walk has started");
+  }
+  if (!ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "K/V prefetch of chunk " + std::to_string(i) + " that was not offloaded");
+  if (ctx->kv_prefetched[i]) return fail(ctx, SPPO_ERR_STATE, "K/V of chunk " + std::to_string(i) + " already prefetched");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HostSlot& h = ctx->slots[i];
+  fold(ctx->t_h2d_kv[i], ctx->ms_h2d);
+  SPPO_HIP(ctx, hipEventRecord(ctx->ev_call[i], s));
+  SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_call[i], 0));
+  SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_off[i], 0));
+  SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d_kv[i].start, ctx->h2d));
+  const size_t w = bytes_kv_row_block(ctx, i);
+  const size_t pitch = (size_t)ctx->prob.seq_len * ctx->prob.n_kv_heads * ctx->prob.head_dim * ctx->elt;
+  const size_t row_off = (size_t)ctx->off[i] * ctx->prob.n_kv_heads * ctx->prob.head_dim * ctx->elt;
+  char* kd = static_cast<char*>(k) + row_off;
+  char* vd = static_cast<char*>(v) + row_off;
+  if (ctx->prob.batch == 1) {
+    SPPO_HIP(ctx, hipMemcpyAsync(kd, h.k, w, hipMemcpyHostToDevice, ctx->h2d));
+    SPPO_HIP(ctx, hipMemcpyAsync(vd, h.v, w, hipMemcpyHostToDevice, ctx->h2d));
+  } else {
+    SPPO_HIP(ctx, hipMemcpy2DAsync(kd, pitch, h.k, w, w, ctx->prob.batch, hipMemcpyHostToDevice, ctx->h2d));
+    SPPO_HIP(ctx, hipMemcpy2DAsync(vd, pitch, h.v, w, w, ctx->prob.batch, hipMemcpyHostToDevice, ctx->h2d));
+  }
+  SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d_kv[i].stop, ctx->h2d));
+  SPPO_HIP(ctx, hipEventRecord(ctx->ev_kv[i], ctx->h2d));
+  ctx->t_h2d_kv[i].pending = true;
+  ctx->kv_prefetched[i] = 1;
+  ctx->bytes_h2d += 2 * w * ctx->prob.batch;
+  return SPPO_OK;
+}
+
 sppo_status sppo_reset(sppo_ctx* ctx) {
   if (!ctx) return SPPO_ERR_INVALID_ARG;
   ctx->in_bwd = false;
@@ -538,6 +612,7 @@ sppo_status sppo_reset(sppo_ctx* ctx) {
   ctx->next_bwd = -1;
   std::fill(ctx->offloaded.begin(), ctx->offloaded.end(), 0);
   std::fill(ctx->prefetched.begin(), ctx->prefetched.end(), 0);
+  std::fill(ctx->kv_prefetched.begin(), ctx->kv_prefetched.end(), 0);
   return SPPO_OK;
 }
 
@@ -545,7 +620,7 @@ sppo_status sppo_set_kernel_timing(sppo_ctx* ctx, int32_t enable) {
   if (!ctx) return SPPO_ERR_INVALID_ARG;
   if (enable && ctx->t_kern[0].empty()) {
     for (auto& v : ctx->t_kern) {
-      v.assign(ctx->prob.n_chunks, EventPair{});
+      v.assign(2 * (size_t)ctx->prob.n_chunks, EventPair{});
       for (EventPair& p : v) {
         SPPO_HIP(ctx, hipEventCreate(&p.start));
         SPPO_HIP(ctx, hipEventCreate(&p.stop));
@@ -583,6 +658,7 @@ sppo_status sppo_copy_stats(sppo_ctx* ctx, sppo_copy_stats_t* out, int32_t reset
   SPPO_HIP(ctx, hipStreamSynchronize(ctx->h2d));
   for (EventPair& p : ctx->t_d2h) fold(p, ctx->ms_d2h);
   for (EventPair& p : ctx->t_h2d) fold(p, ctx->ms_h2d);
+  for (EventPair& p : ctx->t_h2d_kv) fold(p, ctx->ms_h2d);
   out->bytes_d2h = ctx->bytes_d2h;
   out->bytes_h2d = ctx->bytes_h2d;
   out->ms_d2h = ctx->ms_d2h;

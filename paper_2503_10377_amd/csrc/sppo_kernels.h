@@ -23,11 +23,14 @@ struct ChunkArgs {
   int64_t B, S, c0, c1;
   int Hq, Hkv, D;
   float scale;
-  int accumulate;      // dk/dv: 0 = overwrite rows [0, c1), 1 = add
+  int accumulate;      // dk/dv: 0 = overwrite rows [kv0, kv1), 1 = add
+  int64_t kv0, kv1;    // dkdv: key rows computed, a sub-range of [0, c1)
 };
 
 // Each launcher enqueues one kernel on `stream` and returns the launch
-// status.  The backward of a chunk is pre (Delta), then dkdv, then dq.
+// status.  The backward of a chunk is pre (Delta), then dkdv (one launch for
+// key rows [kv0, kv1); several launches over disjoint ranges give the same
+// result), then dq.
 hipError_t launch_fwd_bf16(const ChunkArgs& a, hipStream_t stream);
 hipError_t launch_bwd_pre_bf16(const ChunkArgs& a, hipStream_t stream);
 hipError_t launch_bwd_dkdv_bf16(const ChunkArgs& a, hipStream_t stream);

@@ -31,8 +31,10 @@ SPPO_BF16 = 1
 SPPO_OFFLOAD_NONE = 0
 SPPO_OFFLOAD_QOL = 1
 SPPO_OFFLOAD_QKVOL = 2
+SPPO_OFFLOAD_QKVOL_EVICT = 3
 
-OFFLOAD_MODES = {"none": SPPO_OFFLOAD_NONE, "qol": SPPO_OFFLOAD_QOL, "qkvol": SPPO_OFFLOAD_QKVOL}
+OFFLOAD_MODES = {"none": SPPO_OFFLOAD_NONE, "qol": SPPO_OFFLOAD_QOL, "qkvol": SPPO_OFFLOAD_QKVOL,
+                 "qkvol_evict": SPPO_OFFLOAD_QKVOL_EVICT}
 
 
 class sppo_problem(ctypes.Structure):
@@ -103,6 +105,7 @@ def lib() -> ctypes.CDLL:
             "sppo_offload_issue": ([P, I32, ctypes.POINTER(sppo_chunk_bufs), VP], ctypes.c_int),
             "sppo_offload_wait": ([P, I32, VP], ctypes.c_int),
             "sppo_prefetch": ([P, I32, ctypes.POINTER(sppo_chunk_bufs), VP], ctypes.c_int),
+            "sppo_prefetch_kv": ([P, I32, VP, VP, VP], ctypes.c_int),
             "sppo_reset": ([P], ctypes.c_int),
             "sppo_sync": ([P], ctypes.c_int),
             "sppo_copy_stats": ([P, ctypes.POINTER(sppo_copy_stats_t), I32], ctypes.c_int),
@@ -237,6 +240,10 @@ def sppo_offload_wait(ctx, i, stream=None):
 
 def sppo_prefetch(ctx, i, dst: sppo_chunk_bufs, stream=None):
     _check(ctx, lib().sppo_prefetch(_handle(ctx), i, ctypes.byref(dst), _stream(stream)))
+
+
+def sppo_prefetch_kv(ctx, i, k, v, stream=None):
+    _check(ctx, lib().sppo_prefetch_kv(_handle(ctx), i, _ptr(k), _ptr(v), _stream(stream)))
 
 
 def sppo_reset(ctx):

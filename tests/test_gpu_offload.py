@@ -6,6 +6,10 @@
   Q/O/LSE are overwritten with NaN; the backward must then read the
   prefetched copies, so results stay bitwise equal (a read of stale or
   not-yet-prefetched memory would surface as NaN).
+* K/V eviction (qkvol_evict): the K/V cache rows of offloaded chunks are
+  overwritten with NaN after the forward walk; the backward of the last
+  chunk must consume the prefetched rows piece by piece, and every result
+  stays bitwise equal to the run without offload.
 * Order/state violations return the documented status and enqueue nothing.
 """
 import sys
@@ -27,11 +31,15 @@ def announce(msg):
     print(f"\n[case] {msg}", file=sys.stderr, flush=True)
 
 
-def run(offload="none", offload_chunks=None, lookahead=2, poison=False, B=1, seed=0):
-    S, Hq, Hkv, D = SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"]
-    announce(f"offload={offload} chunks={offload_chunks} lookahead={lookahead} poison={poison} B={B}")
-    inp = make_inputs(B, S, Hq, Hkv, D, torch.bfloat16, seed=seed, device="cuda")
-    ca = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload=offload)
+def run(offload="none", offload_chunks=None, lookahead=2, poison=False, B=1, seed=0, dtype="bf16",
+        offsets=None, shape=None):
+    S, Hq, Hkv, D = (shape or (SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"]))
+    n = N if offsets is None else len(offsets) - 1
+    announce(f"offload={offload} chunks={offload_chunks} lookahead={lookahead} poison={poison} B={B} "
+             f"dtype={dtype} offsets={offsets} shape={(S, Hq, Hkv, D)}")
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    inp = make_inputs(B, S, Hq, Hkv, D, tdt, seed=seed, device="cuda")
+    ca = ChunkedAttention(B, S, n, Hq, Hkv, D, dtype=dtype, offload=offload, offsets=offsets)
     out = ca.alloc_outputs()
     ca.step(inp, out, offload_chunks=offload_chunks, lookahead=lookahead, poison=poison)
     torch.cuda.synchronize()
@@ -70,6 +78,93 @@ def test_poison_batch2():
     ref, _ = run("none", B=2, seed=3)
     res, _ = run("qkvol", poison=True, B=2, seed=3)
     assert_bitwise(ref, res)
+
+
+def test_evict_is_bitwise_invisible(baseline):
+    res, stats = run("qkvol_evict")
+    assert_bitwise(baseline, res)
+    S, Hq, Hkv, D = SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"]
+    s = S // N
+    per_chunk_h2d = 2 * s * Hq * D * 2 + Hq * s * 4 + 2 * s * Hkv * D * 2
+    assert stats["bytes_h2d"] == (N - 1) * per_chunk_h2d
+    assert stats["n_d2h"] == N - 1 and stats["n_h2d"] == N - 1
+
+
+@pytest.mark.parametrize("lookahead", [0, 2])
+def test_evict_poison_all_chunks(baseline, lookahead):
+    res, _ = run("qkvol_evict", offload_chunks=list(range(N)), lookahead=lookahead, poison=True)
+    assert_bitwise(baseline, res)
+
+
+def test_evict_poison_subset_batch2():
+    ref, _ = run("none", B=2, seed=5)
+    res, _ = run("qkvol_evict", offload_chunks=[0, 2, 3, 6], poison=True, B=2, seed=5)
+    assert_bitwise(ref, res)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_evict_poison_ragged(dtype):
+    """Chunk boundaries off the 128-key block grid: the per-chunk dK/dV
+    launches of the last backward start their key blocks at c_j."""
+    offsets = [0, 77, 300, 301, 1000]
+    shape = (1000, 4, 2, 64)
+    ref, _ = run("none", dtype=dtype, offsets=offsets, shape=shape, seed=7)
+    res, _ = run("qkvol_evict", offload_chunks=[0, 1, 2, 3], dtype=dtype, offsets=offsets, shape=shape,
+                 seed=7, poison=True)
+    assert_bitwise(ref, res)
+
+
+def test_evict_state_errors():
+    S, Hq, Hkv, D = 1024, 2, 2, 64
+    announce("evict state errors")
+    inp = make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=0, device="cuda")
+    q, k, v, do = inp["q"], inp["k"], inp["v"], inp["do"]
+
+    def status_of(fn, *a):
+        try:
+            fn(*a)
+        except L.SppoError as e:
+            return e.status
+        return L.SPPO_OK
+
+    # K/V prefetch on a context that does not evict.
+    ca = ChunkedAttention(1, S, 4, Hq, Hkv, D, dtype="bf16", offload="qkvol")
+    assert status_of(L.sppo_prefetch_kv, ca.ctx, 0, k, v) == L.SPPO_ERR_STATE
+    ca.close()
+
+    ca = ChunkedAttention(1, S, 4, Hq, Hkv, D, dtype="bf16", offload="qkvol_evict")
+    out = ca.alloc_outputs()
+    ctx = ca.ctx
+    qc = [ca.chunk_view(q, i) for i in range(4)]
+    oc = [ca.chunk_view(out["o"], i) for i in range(4)]
+    dc = [ca.chunk_view(do, i) for i in range(4)]
+    dqc = [ca.chunk_view(out["dq"], i) for i in range(4)]
+    lse = out["lse"]
+    bufs = lambda i: L.chunk_bufs(q=qc[i], o=oc[i], lse=lse[i], k=k, v=v)  # noqa: E731
+    bwd = lambda i: L.sppo_attn_bwd_chunk(ctx, i, qc[i], k, v, oc[i], lse[i], dc[i], dqc[i],  # noqa: E731
+                                          out["dk"], out["dv"])
+    for i in range(4):
+        L.sppo_attn_fwd_chunk(ctx, i, qc[i], k, v, oc[i], lse[i])
+        if i < 3:
+            L.sppo_offload_issue(ctx, i, bufs(i))
+        if i == 1:
+            # the forward walk is not over yet
+            assert status_of(L.sppo_prefetch_kv, ctx, 0, k, v) == L.SPPO_ERR_STATE
+    assert status_of(L.sppo_prefetch_kv, ctx, 3, k, v) == L.SPPO_ERR_STATE  # never offloaded
+    L.sppo_prefetch_kv(ctx, 2, k, v)
+    L.sppo_prefetch_kv(ctx, 1, k, v)
+    assert status_of(L.sppo_prefetch_kv, ctx, 1, k, v) == L.SPPO_ERR_STATE  # twice
+    assert status_of(bwd, 3) == L.SPPO_ERR_STATE                              # chunk 0's K/V missing
+    L.sppo_prefetch_kv(ctx, 0, k, v)
+    bwd(3)
+    assert status_of(L.sppo_prefetch_kv, ctx, 0, k, v) == L.SPPO_ERR_STATE  # backward started
+    for i in (2, 1, 0):
+        L.sppo_prefetch(ctx, i, bufs(i))
+        bwd(i)
+    torch.cuda.synchronize()
+    ref, _ = run("none", shape=(S, Hq, Hkv, D), offsets=[0, 256, 512, 768, 1024], seed=0)
+    assert torch.equal(out["dk"], ref["dk"]) and torch.equal(out["dq"], ref["dq"])
+    ca.close()
 
 
 def test_copy_bytes_match_the_offload_set():

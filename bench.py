@@ -17,6 +17,13 @@ Reported (one JSON line):
                  step without offload and T_copy the event-timed copy busy
                  time per step; the same for the K/V-evicting walk under
                  offload.evict
+  ms_per_step_median / _min   over the K headline steps (an event between
+                 steps)
+  offload.per_chunk_exposed_ms   per forward / backward chunk, duration with
+                 offload minus without (one marked step of each)
+  offload.link   the library's copy path alone (sppo_link_probe, 1 GiB):
+                 GB/s device->host, host->device and both at once; with it
+                 copy_iso_ms_per_step and hidden_pct_vs_iso
   roofline       the dominant kernel (largest summed time), from HIP events
                  around every launch on the compute stream in K further timed
                  steps (kept out of the headline steps)
@@ -173,22 +180,26 @@ def main():
         L.sppo_set_kernel_timing(c.ctx, timing)
         L.sppo_kernel_times(c.ctx, reset_after=True)
         st = torch.cuda.current_stream()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
         torch.cuda.synchronize()
-        e0.record(st)
-        for _ in range(steps):
+        ev[0].record(st)
+        for n in range(steps):
             c.step(inp, out, lookahead=args.lookahead)
-        e1.record(st)
+            ev[n + 1].record(st)
         torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / steps
+        ms = ev[0].elapsed_time(ev[steps]) / steps
+        step_times.append([ev[n].elapsed_time(ev[n + 1]) for n in range(steps)])
         kt = L.sppo_kernel_times(c.ctx, reset_after=True)
         cs = L.sppo_copy_stats(c.ctx, reset_after=True) if c.offload != L.SPPO_OFFLOAD_NONE else None
         L.sppo_set_kernel_timing(c.ctx, False)
         return ms, kt, cs
 
+    step_times = []
+
     print(f"[bench] workload={args.workload} steps={args.steps} warmup={args.warmup}", file=sys.stderr, flush=True)
     # Headline: exactly K timed steps, no per-kernel events in the stream.
     ms_on, _, cs = timed(ca, args.steps, False)
+    steps_on = sorted(step_times[-1])
     print(f"[bench] ms/step={ms_on:.2f}", file=sys.stderr, flush=True)
     # Per-kernel durations for the roofline: K more steps with HIP events
     # around every launch (the events cost a little time, so they are kept
@@ -204,6 +215,8 @@ def main():
     tflops = flops["total"] / (ms_on * 1e-3) / 1e12
     res["value"] = tflops
     res["pct_peak"] = 100.0 * tflops / PEAK_BF16_TFLOPS
+    res["ms_per_step_median"] = steps_on[len(steps_on) // 2]
+    res["ms_per_step_min"] = steps_on[0]
     res["tokens_per_s"] = S / (ms_on * 1e-3)
     res["config"] = {
         "workload": f"chunked causal attention fwd+bwd, batch {B}, seq {S} in {N} chunks of {S // N}, "
@@ -236,6 +249,17 @@ def main():
         if not args.no_offload_compare:
             ca_off = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="none")
             ms_off, _, _ = timed(ca_off, steps, False)
+            # Per-chunk exposed time: one more step of each with an event at
+            # every chunk boundary; exposed = duration with offload minus
+            # duration without, per forward and per backward chunk.
+            spans = {}
+            for name, c in (("on", ca), ("off", ca_off)):
+                marks = []
+                c.step(inp, out, lookahead=args.lookahead, marks=marks)
+                torch.cuda.synchronize()
+                spans[name] = {marks[n][0]: marks[n][1].elapsed_time(marks[n + 1][1]) for n in range(len(marks) - 1)}
+            off["per_chunk_exposed_ms"] = {
+                ph: [round(spans["on"][(ph, i)] - spans["off"][(ph, i)], 3) for i in range(N)] for ph in ("fwd", "bwd")}
             ca_off.close()
             exposed = max(0.0, ms_on - ms_off)
             off["ms_per_step_no_offload"] = ms_off
@@ -253,6 +277,15 @@ def main():
                     "ms_per_step": ms_evict, "bytes_h2d_per_step": cs_ev["bytes_h2d"] / steps,
                     "copy_ms_per_step": copy_ev, "exposed_ms_per_step": exp_ev,
                     "hidden_pct": 100.0 * max(0.0, min(1.0, 1.0 - exp_ev / copy_ev)) if copy_ev > 0 else None}
+        # Host-link rates of the library's copy path with nothing else
+        # running (1 GiB each way, and both ways at once); T_copy_iso is the
+        # step's copy volume at those rates.
+        link = L.sppo_link_probe(ca.ctx, 1 << 30)
+        iso_ms = (cs["bytes_d2h"] / link["d2h_GBps"] + cs["bytes_h2d"] / link["h2d_GBps"]) / 1e6 / steps
+        off["link"] = link
+        off["copy_iso_ms_per_step"] = iso_ms
+        if "exposed_ms_per_step" in off:
+            off["hidden_pct_vs_iso"] = 100.0 * max(0.0, min(1.0, 1.0 - off["exposed_ms_per_step"] / iso_ms))
         res["offload"] = off
         res["offload_hidden_pct"] = off.get("hidden_pct")
     ca.close()

@@ -218,6 +218,20 @@ sppo_status sppo_sync(sppo_ctx* ctx);
  * `reset_after` != 0 zeroes them afterwards. */
 sppo_status sppo_copy_stats(sppo_ctx* ctx, sppo_copy_stats_t* out, int32_t reset_after);
 
+/* Host-link rates of the context's own copy path, measured in isolation
+ * (the "T_copy_iso" of the offload-hidden figure): allocates a device buffer
+ * and a page-locked host buffer of `bytes` each, then times, on the
+ * context's copy streams with events, one device->host copy, one
+ * host->device copy, and both at once; frees the buffers and returns GB/s
+ * (1e9 bytes per second).  Blocks the host.  Errors: INVALID_ARG (bytes <
+ * 1 MiB), OOM, HIP. */
+typedef struct {
+  double d2h_GBps;     /* device->host alone                               */
+  double h2d_GBps;     /* host->device alone                               */
+  double duplex_GBps;  /* both directions at once, bytes of both / time    */
+} sppo_link_rates_t;
+sppo_status sppo_link_probe(sppo_ctx* ctx, size_t bytes, sppo_link_rates_t* out);
+
 /* Enable (1) or disable (0) per-kernel timing: while enabled, every kernel
  * launch is bracketed by two events on the caller's stream.  Creates the
  * events on first use. */

@@ -81,9 +81,10 @@ class ChunkedAttention:
             return []
         return list(range(self.N - 1))
 
-    def step(self, inp, out, offload_chunks=None, lookahead=2, poison=False, stream=None):
-        """One forward + backward pass over all chunks.  Returns the chunk
-        lists of the B > 1 staging buffers (None for B = 1)."""
+    def step(self, inp, out, offload_chunks=None, lookahead=2, poison=False, stream=None, marks=None):
+        """One forward + backward pass over all chunks.  With ``marks`` (a
+        list), timing events are recorded on the stream before each chunk's
+        forward and backward and at the end, appended as (label, event)."""
         if offload_chunks is None:
             offload_chunks = self.default_offload_chunks()
         offl = set(offload_chunks)
@@ -94,7 +95,15 @@ class ChunkedAttention:
         oc = [self.chunk_view(out["o"], i) for i in range(self.N)]
         dqc = [self.chunk_view(out["dq"], i) for i in range(self.N)]
         lse = out["lse"]
+
+        def mark(label):
+            if marks is not None:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record(s)
+                marks.append((label, e))
+
         for i in range(self.N):
+            mark(("fwd", i))
             L.sppo_attn_fwd_chunk(self.ctx, i, qc[i], k, v, oc[i], lse[i], s)
             if i in offl:
                 bufs = L.chunk_bufs(q=qc[i], o=oc[i], lse=lse[i], k=k, v=v)
@@ -128,8 +137,10 @@ class ChunkedAttention:
                 j = pending[nxt]
                 L.sppo_prefetch(self.ctx, j, L.chunk_bufs(q=qc[j], o=oc[j], lse=lse[j]), s)
                 nxt += 1
+            mark(("bwd", i))
             L.sppo_attn_bwd_chunk(self.ctx, i, qc[i], k, v, oc[i], lse[i], dc[i], dqc[i],
                                   out["dk"], out["dv"], s)
+        mark(("end", -1))
         if self.B > 1:
             for i in range(self.N):
                 c0, c1 = self.offsets[i], self.offsets[i + 1]

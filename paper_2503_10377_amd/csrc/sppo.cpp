@@ -616,6 +616,54 @@ sppo_status sppo_reset(sppo_ctx* ctx) {
   return SPPO_OK;
 }
 
+sppo_status sppo_link_probe(sppo_ctx* ctx, size_t bytes, sppo_link_rates_t* out) {
+  if (!ctx || !out) return SPPO_ERR_INVALID_ARG;
+  if (bytes < (size_t(1) << 20)) return fail(ctx, SPPO_ERR_INVALID_ARG, "link probe needs at least 1 MiB");
+  void* dev = nullptr;
+  void* host = nullptr;
+  hipEvent_t ev[6] = {};
+  hipError_t e = hipMalloc(&dev, bytes);
+  if (e == hipSuccess) e = hipHostMalloc(&host, bytes, hipHostMallocDefault);
+  for (int k = 0; k < 6 && e == hipSuccess; ++k) e = hipEventCreate(&ev[k]);
+  float ms[3] = {};
+  if (e == hipSuccess) e = hipMemset(dev, 0, bytes);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->d2h);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->h2d);
+  // D2H alone, H2D alone (each on its own stream), then both at once.
+  if (e == hipSuccess) e = hipEventRecord(ev[0], ctx->d2h);
+  if (e == hipSuccess) e = copy_d2h(host, dev, bytes, ctx->d2h);
+  if (e == hipSuccess) e = hipEventRecord(ev[1], ctx->d2h);
+  if (e == hipSuccess) e = hipEventSynchronize(ev[1]);
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms[0], ev[0], ev[1]);
+  if (e == hipSuccess) e = hipEventRecord(ev[2], ctx->h2d);
+  if (e == hipSuccess) e = hipMemcpyAsync(dev, host, bytes, hipMemcpyHostToDevice, ctx->h2d);
+  if (e == hipSuccess) e = hipEventRecord(ev[3], ctx->h2d);
+  if (e == hipSuccess) e = hipEventSynchronize(ev[3]);
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms[1], ev[2], ev[3]);
+  // Duplex: the halves of each buffer move in opposite directions.
+  const size_t half = bytes / 2;
+  if (e == hipSuccess) e = hipEventRecord(ev[4], ctx->d2h);
+  if (e == hipSuccess) e = hipStreamWaitEvent(ctx->h2d, ev[4], 0);
+  if (e == hipSuccess) e = copy_d2h(host, dev, half, ctx->d2h);
+  if (e == hipSuccess) e = hipMemcpyAsync(static_cast<char*>(dev) + half, static_cast<char*>(host) + half, half,
+                                          hipMemcpyHostToDevice, ctx->h2d);
+  if (e == hipSuccess) e = hipEventRecord(ev[5], ctx->h2d);
+  if (e == hipSuccess) e = hipStreamWaitEvent(ctx->d2h, ev[5], 0);
+  if (e == hipSuccess) e = hipEventRecord(ev[5], ctx->d2h);
+  if (e == hipSuccess) e = hipEventSynchronize(ev[5]);
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms[2], ev[4], ev[5]);
+  for (hipEvent_t x : ev) {
+    if (x) (void)hipEventDestroy(x);
+  }
+  if (host) (void)hipHostFree(host);
+  if (dev) (void)hipFree(dev);
+  if (e != hipSuccess) return hip_fail(ctx, e, "link probe");
+  out->d2h_GBps = bytes / (ms[0] * 1e6);
+  out->h2d_GBps = bytes / (ms[1] * 1e6);
+  out->duplex_GBps = 2.0 * half / (ms[2] * 1e6);
+  return SPPO_OK;
+}
+
 sppo_status sppo_set_kernel_timing(sppo_ctx* ctx, int32_t enable) {
   if (!ctx) return SPPO_ERR_INVALID_ARG;
   if (enable && ctx->t_kern[0].empty()) {

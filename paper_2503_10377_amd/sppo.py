@@ -80,6 +80,10 @@ class sppo_kernel_times_t(ctypes.Structure):
     _fields_ = [("ms", ctypes.c_double * 4), ("launches", ctypes.c_int32 * 4)]
 
 
+class sppo_link_rates_t(ctypes.Structure):
+    _fields_ = [("d2h_GBps", ctypes.c_double), ("h2d_GBps", ctypes.c_double), ("duplex_GBps", ctypes.c_double)]
+
+
 class SppoError(RuntimeError):
     def __init__(self, status: int, message: str):
         self.status = status
@@ -110,6 +114,7 @@ def lib() -> ctypes.CDLL:
             "sppo_sync": ([P], ctypes.c_int),
             "sppo_copy_stats": ([P, ctypes.POINTER(sppo_copy_stats_t), I32], ctypes.c_int),
             "sppo_set_kernel_timing": ([P, I32], ctypes.c_int),
+            "sppo_link_probe": ([P, ctypes.c_size_t, ctypes.POINTER(sppo_link_rates_t)], ctypes.c_int),
             "sppo_kernel_times": ([P, ctypes.POINTER(sppo_kernel_times_t), I32], ctypes.c_int),
             "sppo_get_offsets": ([P, ctypes.POINTER(ctypes.c_int64), I32], ctypes.c_int),
             "sppo_last_error": ([P], ctypes.c_char_p),
@@ -268,6 +273,12 @@ def sppo_kernel_times(ctx, reset_after=False) -> dict:
     out = sppo_kernel_times_t()
     _check(ctx, lib().sppo_kernel_times(_handle(ctx), ctypes.byref(out), 1 if reset_after else 0))
     return {k: {"ms": out.ms[n], "launches": out.launches[n]} for n, k in enumerate(KERNELS)}
+
+
+def sppo_link_probe(ctx, nbytes) -> dict:
+    out = sppo_link_rates_t()
+    _check(ctx, lib().sppo_link_probe(_handle(ctx), nbytes, ctypes.byref(out)))
+    return {"d2h_GBps": out.d2h_GBps, "h2d_GBps": out.h2d_GBps, "duplex_GBps": out.duplex_GBps}
 
 
 def sppo_get_offsets(ctx) -> list[int]:

@@ -27,6 +27,7 @@ def test_struct_layouts_match_c():
     assert ctypes.sizeof(L.sppo_problem) == 56
     assert ctypes.sizeof(L.sppo_chunk_bufs) == 40
     assert ctypes.sizeof(L.sppo_copy_stats_t) == 40
+    assert ctypes.sizeof(L.sppo_link_rates_t) == 24
 
 
 GOOD = dict(batch=1, seq_len=1024, n_chunks=4, n_q_heads=8, n_kv_heads=2, head_dim=128)

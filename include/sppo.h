@@ -207,6 +207,42 @@ sppo_status sppo_prefetch(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* dst,
  * INVALID_ARG. */
 sppo_status sppo_prefetch_kv(sppo_ctx* ctx, int32_t i, void* k, void* v, void* stream);
 
+/* Sequence-aware offloading (Sec. 5.2, adaptive offloading ratio alpha_i):
+ * offload only the first `rows` rows (0 <= rows <= s_i) of chunk i's
+ * offload set -- a row prefix of Q_i, O_i, LSE_i (and of K_i/V_i with
+ * QKVOL*) -- and keep the rest resident; alpha_i = rows / s_i.  The default
+ * is rows = s_i.  offload_issue, prefetch and prefetch_kv of chunk i then
+ * move that prefix only (rows = 0 moves nothing but still orders the
+ * streams).  Allowed only between walks (after create, reset or bwd(0)).
+ * Errors: INVALID_ARG (index, rows out of range), STATE (mid-walk). */
+sppo_status sppo_set_offload_rows(sppo_ctx* ctx, int32_t i, int64_t rows);
+
+/* The offloaded row prefix of every chunk (n_chunks values). */
+sppo_status sppo_get_offload_rows(const sppo_ctx* ctx, int64_t* out, int32_t capacity);
+
+/* FLOPs-balanced partition (Sec. 3, computation imbalance of causal
+ * attention; Sec. 5.2, FLOPs-based partition): chunk k of a causal
+ * sequence covers about S^2 (2k+1) / (2N^2) of the S^2/2 visible (query,
+ * key) pairs, so equal work per chunk needs c_k = S sqrt(k/N): long chunks
+ * first, shorter ones later.  Writes N+1 offsets to out, each interior
+ * offset rounded to a multiple of `align` and every chunk at least `align`
+ * rows long.  Pure host function.  Errors: INVALID_ARG (S < N * align,
+ * null out, N < 1, align < 1). */
+sppo_status sppo_balanced_offsets(int64_t seq_len, int32_t n_chunks, int64_t align, int64_t* out);
+
+/* Offload plan of sequence-aware offloading (Sec. 5.2): the copy of chunk i
+ * should take no longer than the compute it overlaps, t_overlap_ms[i]
+ * (normally the forward of chunk i+1), so with a device->host rate of
+ * bw_GBps and bytes_per_row bytes of offload set per token row,
+ *   rows_i = min(s_i, floor(bw * t_overlap_i / bytes_per_row)),
+ * rounded down to a multiple of `align` when below s_i; the last chunk gets
+ * rows = 0.  alpha_i = rows_i / s_i; alpha_i * A_i is then bounded by the
+ * bytes the link moves in t_overlap_i.  Pure host function.  Errors:
+ * INVALID_ARG. */
+sppo_status sppo_plan_offload_rows(const int64_t* offsets, int32_t n_chunks, double bytes_per_row,
+                                   double bw_GBps, const double* t_overlap_ms, int64_t align,
+                                   int64_t* rows_out);
+
 /* Abandon the current forward/backward walk (e.g. after a forward-only run):
  * the next call must be fwd(0).  Clears per-chunk offload state. */
 sppo_status sppo_reset(sppo_ctx* ctx);

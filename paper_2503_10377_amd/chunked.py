@@ -76,6 +76,24 @@ class ChunkedAttention:
         return torch.cat(out["lse"], dim=2)
 
     # ---------------------------------------------------------- the walk
+    def set_offload_rows(self, rows):
+        """Offloaded row prefix per chunk (sequence-aware offloading); the
+        rest of each chunk stays resident."""
+        for i, r in enumerate(rows):
+            L.sppo_set_offload_rows(self.ctx, i, r)
+
+    def offload_rows(self):
+        return L.sppo_get_offload_rows(self.ctx)
+
+    def offload_bytes_per_row(self):
+        """Bytes of the offload set per token row (Q, O, LSE; plus K, V in
+        the QKVOL modes), all batch entries."""
+        elt = 2 if self.torch_dtype == torch.bfloat16 else 4
+        b = 2 * self.Hq * self.D * elt + 4 * self.Hq
+        if self.offload in (L.SPPO_OFFLOAD_QKVOL, L.SPPO_OFFLOAD_QKVOL_EVICT):
+            b += 2 * self.Hkv * self.D * elt
+        return self.B * b
+
     def default_offload_chunks(self):
         if self.offload == L.SPPO_OFFLOAD_NONE:
             return []
@@ -95,6 +113,7 @@ class ChunkedAttention:
         oc = [self.chunk_view(out["o"], i) for i in range(self.N)]
         dqc = [self.chunk_view(out["dq"], i) for i in range(self.N)]
         lse = out["lse"]
+        rows = self.offload_rows() if poison else None
 
         def mark(label):
             if marks is not None:
@@ -110,12 +129,14 @@ class ChunkedAttention:
                 L.sppo_offload_issue(self.ctx, i, bufs, s)
                 if poison:
                     # Test hook: once the copy has landed on the host, the
-                    # device copies are dead; overwrite them with NaN.
+                    # offloaded rows on the device are dead; overwrite them
+                    # with NaN (the resident remainder stays intact).
                     L.sppo_offload_wait(self.ctx, i, s)
+                    r = rows[i]
                     with torch.cuda.stream(s):
-                        qc[i].fill_(float("nan"))
-                        oc[i].fill_(float("nan"))
-                        lse[i].fill_(float("nan"))
+                        qc[i][:, :r].fill_(float("nan"))
+                        oc[i][:, :r].fill_(float("nan"))
+                        lse[i][:, :, :r].fill_(float("nan"))
         if self.offload == L.SPPO_OFFLOAD_QKVOL_EVICT:
             kv_chunks = sorted(offl, reverse=True)
             if poison:
@@ -125,9 +146,9 @@ class ChunkedAttention:
                     L.sppo_offload_wait(self.ctx, j, s)
                 with torch.cuda.stream(s):
                     for j in kv_chunks:
-                        c0, c1 = self.offsets[j], self.offsets[j + 1]
-                        k[:, c0:c1].fill_(float("nan"))
-                        v[:, c0:c1].fill_(float("nan"))
+                        c0 = self.offsets[j]
+                        k[:, c0:c0 + rows[j]].fill_(float("nan"))
+                        v[:, c0:c0 + rows[j]].fill_(float("nan"))
             for j in kv_chunks:
                 L.sppo_prefetch_kv(self.ctx, j, k, v, s)
         pending = sorted(offl, reverse=True)

@@ -65,6 +65,7 @@ struct sppo_ctx {
   std::vector<hipEvent_t> ev_fwd, ev_off, ev_call, ev_pf, ev_kv;
   std::vector<EventPair> t_d2h, t_h2d, t_h2d_kv;
   std::vector<uint8_t> offloaded, prefetched, kv_prefetched;
+  std::vector<int64_t> rows;  // offloaded row prefix of each chunk (default s_i)
   bool in_bwd = false;
   int next_fwd = 0, next_bwd = -1;
   uint64_t bytes_d2h = 0, bytes_h2d = 0;
@@ -166,6 +167,65 @@ hipError_t copy_d2h(void* dst, const void* src, size_t n, hipStream_t s) {
     e = hipMemcpy2DAsync(static_cast<char*>(dst) + rows * W, tail, static_cast<const char*>(src) + rows * W,
                          tail, tail, 1, hipMemcpyDeviceToHost, s);
   }
+  return e;
+}
+
+// `height` rows of `width` bytes with the given pitches.  Contiguous spans
+// take one linear copy (device->host through copy_d2h); strided ones a rect
+// copy.
+hipError_t copy_rows(void* dst, size_t dpitch, const void* src, size_t spitch, size_t width, size_t height,
+                     hipMemcpyKind kind, hipStream_t s) {
+  if (width == 0 || height == 0) return hipSuccess;
+  if (height == 1 || (width == dpitch && width == spitch)) {
+    const size_t n = width * height;
+    return kind == hipMemcpyDeviceToHost ? copy_d2h(dst, src, n, s) : hipMemcpyAsync(dst, src, n, kind, s);
+  }
+  return hipMemcpy2DAsync(dst, dpitch, src, spitch, width, height, kind, s);
+}
+
+// Move the first r rows of chunk i's Q, O and LSE between the device
+// buffers and host slot i (the slot mirrors the chunk-local layout):
+//   Q_i, O_i [B, s_i, Hq, D]: B spans of r*Hq*D elements, pitch s_i*Hq*D
+//   LSE_i   [B, Hq, s_i]    : B*Hq spans of r floats, pitch s_i
+// Returns the bytes moved through *bytes.
+hipError_t move_qol(sppo_ctx* c, int i, int64_t r, void* q, void* o, float* lse, bool to_host, hipStream_t s,
+                    uint64_t* bytes) {
+  const size_t row = (size_t)c->prob.n_q_heads * c->prob.head_dim * c->elt;
+  const size_t si = (size_t)chunk_len(c, i), B = (size_t)c->prob.batch, BH = B * c->prob.n_q_heads;
+  const hipMemcpyKind kind = to_host ? hipMemcpyDeviceToHost : hipMemcpyHostToDevice;
+  HostSlot& h = c->slots[i];
+  hipError_t e = hipSuccess;
+  void* dev[2] = {q, o};
+  void* host[2] = {h.q, h.o};
+  for (int t = 0; t < 2 && e == hipSuccess; ++t) {
+    e = to_host ? copy_rows(host[t], si * row, dev[t], si * row, r * row, B, kind, s)
+                : copy_rows(dev[t], si * row, host[t], si * row, r * row, B, kind, s);
+  }
+  if (e == hipSuccess) {
+    const size_t lp = si * sizeof(float), lw = (size_t)r * sizeof(float);
+    e = to_host ? copy_rows(h.lse, lp, lse, lp, lw, BH, kind, s) : copy_rows(lse, lp, h.lse, lp, lw, BH, kind, s);
+  }
+  *bytes = 2 * (uint64_t)r * row * B + (uint64_t)r * sizeof(float) * BH;
+  return e;
+}
+
+// Move the first r rows of chunk i's K/V cache rows ([c_i, c_i + r) of the
+// full [B, S, Hkv, D] tensors) between the device and host slot i (B spans,
+// pitch s_i rows on the host, S rows on the device).
+hipError_t move_kv(sppo_ctx* c, int i, int64_t r, void* k, void* v, bool to_host, hipStream_t s, uint64_t* bytes) {
+  const size_t row = (size_t)c->prob.n_kv_heads * c->prob.head_dim * c->elt;
+  const size_t si = (size_t)chunk_len(c, i), B = (size_t)c->prob.batch, S = (size_t)c->prob.seq_len;
+  const size_t off = (size_t)c->off[i] * row;
+  const hipMemcpyKind kind = to_host ? hipMemcpyDeviceToHost : hipMemcpyHostToDevice;
+  HostSlot& h = c->slots[i];
+  hipError_t e = hipSuccess;
+  char* dev[2] = {static_cast<char*>(k) + off, static_cast<char*>(v) + off};
+  void* host[2] = {h.k, h.v};
+  for (int t = 0; t < 2 && e == hipSuccess; ++t) {
+    e = to_host ? copy_rows(host[t], si * row, dev[t], S * row, r * row, B, kind, s)
+                : copy_rows(dev[t], S * row, host[t], si * row, r * row, B, kind, s);
+  }
+  *bytes = 2 * (uint64_t)r * row * B;
   return e;
 }
 
@@ -328,6 +388,8 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
   c->offloaded.assign(N, 0);
   c->prefetched.assign(N, 0);
   c->kv_prefetched.assign(N, 0);
+  c->rows.resize(N);
+  for (int i = 0; i < N; ++i) c->rows[i] = chunk_len(c, i);
   c->slots.assign(N, HostSlot{});
   if (p->offload != SPPO_OFFLOAD_NONE) {
     for (int i = 0; i < N; ++i) {
@@ -494,31 +556,15 @@ sppo_status sppo_offload_issue(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* 
   if (ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " already offloaded");
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  HostSlot& h = ctx->slots[i];
   fold(ctx->t_d2h[i], ctx->ms_d2h);
   SPPO_HIP(ctx, hipEventRecord(ctx->ev_fwd[i], s));
   SPPO_HIP(ctx, hipStreamWaitEvent(ctx->d2h, ctx->ev_fwd[i], 0));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_d2h[i].start, ctx->d2h));
-  const size_t bq = bytes_q(ctx, i), bl = bytes_lse(ctx, i);
-  SPPO_HIP(ctx, copy_d2h(h.q, src->q, bq, ctx->d2h));
-  SPPO_HIP(ctx, copy_d2h(h.o, src->o, bq, ctx->d2h));
-  SPPO_HIP(ctx, copy_d2h(h.lse, src->lse, bl, ctx->d2h));
-  uint64_t bytes = 2 * bq + bl;
-  if (offload_kv(ctx)) {
-    const size_t w = bytes_kv_row_block(ctx, i);
-    const size_t pitch = (size_t)ctx->prob.seq_len * ctx->prob.n_kv_heads * ctx->prob.head_dim * ctx->elt;
-    const size_t row_off = (size_t)ctx->off[i] * ctx->prob.n_kv_heads * ctx->prob.head_dim * ctx->elt;
-    const char* ks = static_cast<const char*>(src->k) + row_off;
-    const char* vs = static_cast<const char*>(src->v) + row_off;
-    if (ctx->prob.batch == 1) {
-      SPPO_HIP(ctx, copy_d2h(h.k, ks, w, ctx->d2h));
-      SPPO_HIP(ctx, copy_d2h(h.v, vs, w, ctx->d2h));
-    } else {
-      SPPO_HIP(ctx, hipMemcpy2DAsync(h.k, w, ks, pitch, w, ctx->prob.batch, hipMemcpyDeviceToHost, ctx->d2h));
-      SPPO_HIP(ctx, hipMemcpy2DAsync(h.v, w, vs, pitch, w, ctx->prob.batch, hipMemcpyDeviceToHost, ctx->d2h));
-    }
-    bytes += 2 * w * ctx->prob.batch;
-  }
+  const int64_t r = ctx->rows[i];
+  uint64_t bytes = 0, kv_bytes = 0;
+  SPPO_HIP(ctx, move_qol(ctx, i, r, src->q, src->o, src->lse, true, ctx->d2h, &bytes));
+  if (offload_kv(ctx)) SPPO_HIP(ctx, move_kv(ctx, i, r, src->k, src->v, true, ctx->d2h, &kv_bytes));
+  bytes += kv_bytes;
   SPPO_HIP(ctx, hipEventRecord(ctx->t_d2h[i].stop, ctx->d2h));
   SPPO_HIP(ctx, hipEventRecord(ctx->ev_off[i], ctx->d2h));
   ctx->t_d2h[i].pending = true;
@@ -548,21 +594,18 @@ sppo_status sppo_prefetch(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* dst, 
   if (!ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "prefetch of chunk " + std::to_string(i) + " that was not offloaded");
   if (ctx->prefetched[i]) return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " already prefetched");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  HostSlot& h = ctx->slots[i];
   fold(ctx->t_h2d[i], ctx->ms_h2d);
   SPPO_HIP(ctx, hipEventRecord(ctx->ev_call[i], s));
   SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_call[i], 0));
   SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_off[i], 0));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d[i].start, ctx->h2d));
-  const size_t bq = bytes_q(ctx, i), bl = bytes_lse(ctx, i);
-  SPPO_HIP(ctx, hipMemcpyAsync(dst->q, h.q, bq, hipMemcpyHostToDevice, ctx->h2d));
-  SPPO_HIP(ctx, hipMemcpyAsync(dst->o, h.o, bq, hipMemcpyHostToDevice, ctx->h2d));
-  SPPO_HIP(ctx, hipMemcpyAsync(dst->lse, h.lse, bl, hipMemcpyHostToDevice, ctx->h2d));
+  uint64_t bytes = 0;
+  SPPO_HIP(ctx, move_qol(ctx, i, ctx->rows[i], dst->q, dst->o, dst->lse, false, ctx->h2d, &bytes));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d[i].stop, ctx->h2d));
   SPPO_HIP(ctx, hipEventRecord(ctx->ev_pf[i], ctx->h2d));
   ctx->t_h2d[i].pending = true;
   ctx->prefetched[i] = 1;
-  ctx->bytes_h2d += 2 * bq + bl;
+  ctx->bytes_h2d += bytes;
   ctx->n_h2d += 1;
   return SPPO_OK;
 }
@@ -579,29 +622,35 @@ sppo_status sppo_prefetch_kv(sppo_ctx* ctx, int32_t i, void* k, void* v, void* s
   if (!ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "K/V prefetch of chunk " + std::to_string(i) + " that was not offloaded");
   if (ctx->kv_prefetched[i]) return fail(ctx, SPPO_ERR_STATE, "K/V of chunk " + std::to_string(i) + " already prefetched");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  HostSlot& h = ctx->slots[i];
   fold(ctx->t_h2d_kv[i], ctx->ms_h2d);
   SPPO_HIP(ctx, hipEventRecord(ctx->ev_call[i], s));
   SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_call[i], 0));
   SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_off[i], 0));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d_kv[i].start, ctx->h2d));
-  const size_t w = bytes_kv_row_block(ctx, i);
-  const size_t pitch = (size_t)ctx->prob.seq_len * ctx->prob.n_kv_heads * ctx->prob.head_dim * ctx->elt;
-  const size_t row_off = (size_t)ctx->off[i] * ctx->prob.n_kv_heads * ctx->prob.head_dim * ctx->elt;
-  char* kd = static_cast<char*>(k) + row_off;
-  char* vd = static_cast<char*>(v) + row_off;
-  if (ctx->prob.batch == 1) {
-    SPPO_HIP(ctx, hipMemcpyAsync(kd, h.k, w, hipMemcpyHostToDevice, ctx->h2d));
-    SPPO_HIP(ctx, hipMemcpyAsync(vd, h.v, w, hipMemcpyHostToDevice, ctx->h2d));
-  } else {
-    SPPO_HIP(ctx, hipMemcpy2DAsync(kd, pitch, h.k, w, w, ctx->prob.batch, hipMemcpyHostToDevice, ctx->h2d));
-    SPPO_HIP(ctx, hipMemcpy2DAsync(vd, pitch, h.v, w, w, ctx->prob.batch, hipMemcpyHostToDevice, ctx->h2d));
-  }
+  uint64_t bytes = 0;
+  SPPO_HIP(ctx, move_kv(ctx, i, ctx->rows[i], k, v, false, ctx->h2d, &bytes));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d_kv[i].stop, ctx->h2d));
   SPPO_HIP(ctx, hipEventRecord(ctx->ev_kv[i], ctx->h2d));
   ctx->t_h2d_kv[i].pending = true;
   ctx->kv_prefetched[i] = 1;
-  ctx->bytes_h2d += 2 * w * ctx->prob.batch;
+  ctx->bytes_h2d += bytes;
+  return SPPO_OK;
+}
+
+sppo_status sppo_set_offload_rows(sppo_ctx* ctx, int32_t i, int64_t rows) {
+  sppo_status st = check_ctx_index(ctx, i);
+  if (st != SPPO_OK) return st;
+  if (rows < 0 || rows > chunk_len(ctx, i)) {
+    return fail(ctx, SPPO_ERR_INVALID_ARG, "offload rows of chunk " + std::to_string(i) + " outside [0, s_i]");
+  }
+  if (ctx->in_bwd || ctx->next_fwd != 0) return fail(ctx, SPPO_ERR_STATE, "offload rows changed during a walk");
+  ctx->rows[i] = rows;
+  return SPPO_OK;
+}
+
+sppo_status sppo_get_offload_rows(const sppo_ctx* ctx, int64_t* out, int32_t capacity) {
+  if (!ctx || !out || capacity < ctx->prob.n_chunks) return SPPO_ERR_INVALID_ARG;
+  for (int i = 0; i < ctx->prob.n_chunks; ++i) out[i] = ctx->rows[i];
   return SPPO_OK;
 }
 
@@ -717,6 +766,46 @@ sppo_status sppo_copy_stats(sppo_ctx* ctx, sppo_copy_stats_t* out, int32_t reset
     ctx->bytes_d2h = ctx->bytes_h2d = 0;
     ctx->ms_d2h = ctx->ms_h2d = 0.0;
     ctx->n_d2h = ctx->n_h2d = 0;
+  }
+  return SPPO_OK;
+}
+
+sppo_status sppo_balanced_offsets(int64_t seq_len, int32_t n_chunks, int64_t align, int64_t* out) {
+  if (!out || seq_len < 1 || n_chunks < 1 || align < 1 || (int64_t)n_chunks * align > seq_len) {
+    return SPPO_ERR_INVALID_ARG;
+  }
+  const int N = n_chunks;
+  out[0] = 0;
+  out[N] = seq_len;
+  for (int k = 1; k < N; ++k) {
+    const double c = (double)seq_len * std::sqrt((double)k / N);
+    out[k] = (int64_t)std::llround(c / align) * align;
+  }
+  // Every chunk at least `align` rows long: push up from the front, then
+  // down from the back (room exists since N * align <= S).
+  for (int k = 1; k < N; ++k) out[k] = std::max(out[k], out[k - 1] + align);
+  for (int k = N - 1; k >= 1; --k) out[k] = std::min(out[k], out[k + 1] - align);
+  return SPPO_OK;
+}
+
+sppo_status sppo_plan_offload_rows(const int64_t* offsets, int32_t n_chunks, double bytes_per_row, double bw_GBps,
+                                   const double* t_overlap_ms, int64_t align, int64_t* rows_out) {
+  if (!offsets || !t_overlap_ms || !rows_out || n_chunks < 1 || !(bytes_per_row > 0.0) || !(bw_GBps > 0.0) ||
+      align < 1) {
+    return SPPO_ERR_INVALID_ARG;
+  }
+  for (int i = 0; i < n_chunks; ++i) {
+    const int64_t si = offsets[i + 1] - offsets[i];
+    if (si < 1 || !(t_overlap_ms[i] >= 0.0)) return SPPO_ERR_INVALID_ARG;
+    if (i == n_chunks - 1) {
+      rows_out[i] = 0;  // its backward follows its forward directly
+      continue;
+    }
+    // Bytes the link moves while the overlapped compute runs.
+    const double fit = bw_GBps * 1e6 * t_overlap_ms[i] / bytes_per_row;
+    int64_t r = fit >= (double)si ? si : (int64_t)std::floor(fit);
+    if (r < si) r = (r / align) * align;
+    rows_out[i] = r;
   }
   return SPPO_OK;
 }

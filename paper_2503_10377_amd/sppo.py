@@ -115,6 +115,13 @@ def lib() -> ctypes.CDLL:
             "sppo_copy_stats": ([P, ctypes.POINTER(sppo_copy_stats_t), I32], ctypes.c_int),
             "sppo_set_kernel_timing": ([P, I32], ctypes.c_int),
             "sppo_link_probe": ([P, ctypes.c_size_t, ctypes.POINTER(sppo_link_rates_t)], ctypes.c_int),
+            "sppo_set_offload_rows": ([P, I32, ctypes.c_int64], ctypes.c_int),
+            "sppo_get_offload_rows": ([P, ctypes.POINTER(ctypes.c_int64), I32], ctypes.c_int),
+            "sppo_balanced_offsets": ([ctypes.c_int64, I32, ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)],
+                                      ctypes.c_int),
+            "sppo_plan_offload_rows": ([ctypes.POINTER(ctypes.c_int64), I32, ctypes.c_double, ctypes.c_double,
+                                        ctypes.POINTER(ctypes.c_double), ctypes.c_int64,
+                                        ctypes.POINTER(ctypes.c_int64)], ctypes.c_int),
             "sppo_kernel_times": ([P, ctypes.POINTER(sppo_kernel_times_t), I32], ctypes.c_int),
             "sppo_get_offsets": ([P, ctypes.POINTER(ctypes.c_int64), I32], ctypes.c_int),
             "sppo_last_error": ([P], ctypes.c_char_p),
@@ -279,6 +286,41 @@ def sppo_link_probe(ctx, nbytes) -> dict:
     out = sppo_link_rates_t()
     _check(ctx, lib().sppo_link_probe(_handle(ctx), nbytes, ctypes.byref(out)))
     return {"d2h_GBps": out.d2h_GBps, "h2d_GBps": out.h2d_GBps, "duplex_GBps": out.duplex_GBps}
+
+
+def sppo_set_offload_rows(ctx, i, rows):
+    _check(ctx, lib().sppo_set_offload_rows(_handle(ctx), i, int(rows)))
+
+
+def sppo_get_offload_rows(ctx) -> list[int]:
+    n = ctx.problem["n_chunks"]
+    arr = (ctypes.c_int64 * n)()
+    _check(ctx, lib().sppo_get_offload_rows(_handle(ctx), arr, n))
+    return list(arr)
+
+
+def _status_check(st, what):
+    if st != SPPO_OK:
+        raise SppoError(st, what)
+
+
+def sppo_balanced_offsets(seq_len, n_chunks, align=1) -> list[int]:
+    arr = (ctypes.c_int64 * (n_chunks + 1))()
+    _status_check(lib().sppo_balanced_offsets(seq_len, n_chunks, align, arr),
+                  f"balanced offsets S={seq_len} N={n_chunks} align={align}")
+    return list(arr)
+
+
+def sppo_plan_offload_rows(offsets, bytes_per_row, bw_GBps, t_overlap_ms, align=1) -> list[int]:
+    n = len(offsets) - 1
+    if len(t_overlap_ms) != n:
+        raise ValueError("t_overlap_ms needs one value per chunk")
+    off = (ctypes.c_int64 * (n + 1))(*offsets)
+    t = (ctypes.c_double * n)(*t_overlap_ms)
+    rows = (ctypes.c_int64 * n)()
+    _status_check(lib().sppo_plan_offload_rows(off, n, float(bytes_per_row), float(bw_GBps), t, align, rows),
+                  "offload plan")
+    return list(rows)
 
 
 def sppo_get_offsets(ctx) -> list[int]:

@@ -32,7 +32,7 @@ def announce(msg):
 
 
 def run(offload="none", offload_chunks=None, lookahead=2, poison=False, B=1, seed=0, dtype="bf16",
-        offsets=None, shape=None):
+        offsets=None, shape=None, rows=None):
     S, Hq, Hkv, D = (shape or (SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"]))
     n = N if offsets is None else len(offsets) - 1
     announce(f"offload={offload} chunks={offload_chunks} lookahead={lookahead} poison={poison} B={B} "
@@ -40,6 +40,8 @@ def run(offload="none", offload_chunks=None, lookahead=2, poison=False, B=1, see
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     inp = make_inputs(B, S, Hq, Hkv, D, tdt, seed=seed, device="cuda")
     ca = ChunkedAttention(B, S, n, Hq, Hkv, D, dtype=dtype, offload=offload, offsets=offsets)
+    if rows is not None:
+        ca.set_offload_rows(rows)
     out = ca.alloc_outputs()
     ca.step(inp, out, offload_chunks=offload_chunks, lookahead=lookahead, poison=poison)
     torch.cuda.synchronize()
@@ -164,6 +166,45 @@ def test_evict_state_errors():
     torch.cuda.synchronize()
     ref, _ = run("none", shape=(S, Hq, Hkv, D), offsets=[0, 256, 512, 768, 1024], seed=0)
     assert torch.equal(out["dk"], ref["dk"]) and torch.equal(out["dq"], ref["dq"])
+    ca.close()
+
+
+@pytest.mark.parametrize("mode,B", [("qol", 1), ("qkvol", 1), ("qkvol_evict", 1), ("qkvol_evict", 2)])
+def test_partial_offload_rows(mode, B):
+    """Sequence-aware offloading: only a row prefix of each chunk leaves the
+    device (poisoned after its copy lands); the rest stays resident."""
+    S, Hq, Hkv, D = SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"]
+    s = S // N
+    rows = [s // 2, 0, 100, s, 37, s - 1, 1, 64]
+    ref = run("none", B=B, seed=9)[0]
+    res, stats = run(mode, offload_chunks=list(range(N)), poison=True, B=B, seed=9, rows=rows)
+    assert_bitwise(ref, res)
+    per_row = 2 * Hq * D * 2 + 4 * Hq + (2 * Hkv * D * 2 if mode != "qol" else 0)
+    assert stats["bytes_d2h"] == B * sum(rows) * per_row
+    assert stats["bytes_h2d"] == B * sum(rows) * per_row - (0 if mode == "qkvol_evict" else
+                                                            B * sum(rows) * (per_row - 2 * Hq * D * 2 - 4 * Hq))
+
+
+def test_offload_rows_errors():
+    announce("offload rows errors")
+    S, Hq, Hkv, D = 1024, 2, 2, 64
+    inp = make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=0, device="cuda")
+    ca = ChunkedAttention(1, S, 4, Hq, Hkv, D, dtype="bf16", offload="qol")
+    for i, r in ((0, -1), (0, 257), (4, 0)):
+        with pytest.raises(L.SppoError) as ei:
+            L.sppo_set_offload_rows(ca.ctx, i, r)
+        assert ei.value.status == L.SPPO_ERR_INVALID_ARG
+    L.sppo_set_offload_rows(ca.ctx, 1, 256)
+    out = ca.alloc_outputs()
+    L.sppo_attn_fwd_chunk(ca.ctx, 0, ca.chunk_view(inp["q"], 0), inp["k"], inp["v"], ca.chunk_view(out["o"], 0),
+                          out["lse"][0])
+    with pytest.raises(L.SppoError) as ei:
+        L.sppo_set_offload_rows(ca.ctx, 1, 128)  # mid-walk
+    assert ei.value.status == L.SPPO_ERR_STATE
+    L.sppo_reset(ca.ctx)
+    L.sppo_set_offload_rows(ca.ctx, 1, 128)
+    assert ca.offload_rows() == [256, 128, 256, 256]
+    torch.cuda.synchronize()
     ca.close()
 
 

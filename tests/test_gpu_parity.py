@@ -9,6 +9,7 @@ import pytest
 import torch
 
 import oracle
+from paper_2503_10377_amd import sppo as L
 from paper_2503_10377_amd.chunked import ChunkedAttention
 from paper_2503_10377_amd.inputs import make_inputs
 from parity import check_all, to_np
@@ -23,7 +24,7 @@ def announce(msg):
 
 
 def run_case(B, S, Hq, Hkv, D, dtype, N=None, offsets=None, seed=0, kind="randn",
-             offload="none", lookahead=2, poison=False):
+             offload="none", lookahead=2, poison=False, rows=None):
     if offsets is None:
         offsets = list(oracle.equal_offsets(S, N))
     N = len(offsets) - 1
@@ -32,6 +33,8 @@ def run_case(B, S, Hq, Hkv, D, dtype, N=None, offsets=None, seed=0, kind="randn"
     inp = make_inputs(B, S, Hq, Hkv, D, TORCH_DT[dtype], seed=seed, device="cuda", kind=kind)
     host = {n: to_np(t) for n, t in inp.items()}  # taken before the HIP path runs
     ca = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype=dtype, offsets=offsets, offload=offload)
+    if rows is not None:
+        ca.set_offload_rows(rows)
     out = ca.alloc_outputs()
     ca.step(inp, out, lookahead=lookahead, poison=poison)
     torch.cuda.synchronize()
@@ -71,6 +74,19 @@ def test_bf16_ragged_offsets(D):
     # Chunk lengths 77, 223, 1, 699: tails inside every tile size, a
     # one-row chunk, and chunk boundaries off the tile grid.
     gpu, ref, off = run_case(1, 1000, 2, 1, D, "bf16", offsets=[0, 77, 300, 301, 1000], seed=2)
+    check_all(gpu, ref, "bf16", off)
+
+
+def test_bf16_balanced_partition_partial_offload():
+    """FLOPs-balanced boundaries (long chunks first, c_k = S sqrt(k/N) on a
+    64-row grid) with a sequence-aware partial offload: only a row prefix
+    of each chunk leaves the device (and is poisoned there)."""
+    S, N = 3072, 6
+    offsets = L.sppo_balanced_offsets(S, N, 64)
+    lens = [b - a for a, b in zip(offsets, offsets[1:])]
+    rows = [lens[0] // 3, lens[1] - 5, 0, 64, lens[4], 0]
+    gpu, ref, off = run_case(1, S, 4, 2, 128, "bf16", offsets=offsets, seed=11, offload="qkvol",
+                             poison=True, rows=rows)
     check_all(gpu, ref, "bf16", off)
 
 

@@ -21,6 +21,11 @@ Reported (one JSON line):
                  steps)
   offload.per_chunk_exposed_ms   per forward / backward chunk, duration with
                  offload minus without (one marked step of each)
+  offload_policy equal vs FLOPs-balanced chunk boundaries, each with the full
+                 offload set and with the sequence-aware plan (row prefix per
+                 chunk sized so its copy fits under the next chunk's forward
+                 at the isolated link rate): step time, hidden fraction,
+                 bytes, and the modelled peak of offloadable activations
   offload.link   the library's copy path alone (sppo_link_probe, 1 GiB):
                  GB/s device->host, host->device and both at once; with it
                  copy_iso_ms_per_step and hidden_pct_vs_iso
@@ -149,6 +154,7 @@ def main():
                     help="only run a device copy of BYTES (counter calibration) and exit")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-offload-compare", action="store_true")
+    ap.add_argument("--no-policy", action="store_true", help="skip the partition / offload-ratio comparison")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -172,9 +178,10 @@ def main():
     out = ca.alloc_outputs()
     flops = algorithmic_flops(ca.offsets, B, Hq, D)
 
-    def timed(c, steps, timing):
+    def timed(c, steps, timing, o=None):
+        o = out if o is None else o
         for _ in range(args.warmup):
-            c.step(inp, out, lookahead=args.lookahead)
+            c.step(inp, o, lookahead=args.lookahead)
         torch.cuda.synchronize()
         L.sppo_copy_stats(c.ctx, reset_after=True)
         L.sppo_set_kernel_timing(c.ctx, timing)
@@ -184,7 +191,7 @@ def main():
         torch.cuda.synchronize()
         ev[0].record(st)
         for n in range(steps):
-            c.step(inp, out, lookahead=args.lookahead)
+            c.step(inp, o, lookahead=args.lookahead)
             ev[n + 1].record(st)
         torch.cuda.synchronize()
         ms = ev[0].elapsed_time(ev[steps]) / steps
@@ -195,6 +202,78 @@ def main():
         return ms, kt, cs
 
     step_times = []
+
+    def chunk_fwd_ms(c, o):
+        """Forward duration of each chunk, from one step with an event at
+        every chunk boundary."""
+        marks = []
+        c.step(inp, o, lookahead=args.lookahead, marks=marks)
+        torch.cuda.synchronize()
+        span = {marks[n][0]: marks[n][1].elapsed_time(marks[n + 1][1]) for n in range(len(marks) - 1)}
+        return [span[("fwd", i)] for i in range(c.N)]
+
+    def modelled_peak_bytes(t_fwd, lens, rows, copy_row, freed_row, bw_GBps):
+        """Peak device bytes of the chunks' offloadable activations (Q, O,
+        LSE) during the forward walk, when each offloaded prefix is freed as
+        soon as its copy lands: copies leave in chunk order (one FIFO
+        stream), copy i starts at max(end of fwd i, end of copy i-1) and
+        takes rows_i * copy_row / bw; chunk i's set is live from the start
+        of fwd i.  Measured forward times and link rate, modelled frees."""
+        bw = bw_GBps * 1e6  # bytes per ms
+        start = [0.0]
+        for t in t_fwd:
+            start.append(start[-1] + t)
+        end, prev = [], 0.0
+        for i, r in enumerate(rows):
+            begin = max(start[i + 1], prev)
+            prev = begin + r * copy_row / bw
+            end.append(prev)
+        peak = 0.0
+        for i in range(len(lens)):
+            live = sum(lens[j] * freed_row for j in range(i + 1))
+            freed = sum(rows[j] * freed_row for j in range(i) if end[j] <= start[i])
+            peak = max(peak, live - freed)
+        return peak
+
+    def policy_compare(bw_GBps):
+        """Sequence-aware offloading (NEXT-1): equal vs FLOPs-balanced chunk
+        boundaries, each with the full offload set and with the planned row
+        prefix per chunk (copy of chunk i bounded by the forward of chunk
+        i+1 at the isolated link rate)."""
+        result = {}
+        freed_row = B * (2 * Hq * D * 2 + 4 * Hq)
+        for part in ("equal", "balanced"):
+            offs = None if part == "equal" else L.sppo_balanced_offsets(S, N, 128)
+            c_none = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offsets=offs, offload="none")
+            o = c_none.alloc_outputs()
+            ms_none, _, _ = timed(c_none, steps, False, o)
+            t_fwd = chunk_fwd_ms(c_none, o)
+            c_none.close()
+            c_on = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offsets=offs, offload="qkvol")
+            lens = [c_on.chunk_len(i) for i in range(N)]
+            copy_row = c_on.offload_bytes_per_row()
+            plan = L.sppo_plan_offload_rows(c_on.offsets, copy_row, bw_GBps, t_fwd[1:] + [0.0], 128)
+            entry = {"offsets": c_on.offsets, "ms_per_step_no_offload": ms_none, "fwd_ms_per_chunk": t_fwd}
+            for name, rows in (("full", lens[:-1] + [0]), ("plan", plan)):
+                c_on.set_offload_rows(rows)
+                ms, _, cs_p = timed(c_on, steps, False, o)
+                copy_p = (cs_p["ms_d2h"] + cs_p["ms_h2d"]) / steps
+                exp_p = max(0.0, ms - ms_none)
+                entry[name] = {
+                    "rows": rows, "alpha": [round(r / n, 4) for r, n in zip(rows, lens)],
+                    "ms_per_step": ms, "tflops": flops["total"] / (ms * 1e-3) / 1e12,
+                    "bytes_d2h_per_step": cs_p["bytes_d2h"] / steps, "copy_ms_per_step": copy_p,
+                    "exposed_ms_per_step": exp_p,
+                    "hidden_pct": 100.0 * max(0.0, min(1.0, 1.0 - exp_p / copy_p)) if copy_p > 0 else None,
+                    "modelled_peak_activation_GiB": modelled_peak_bytes(
+                        t_fwd, lens, rows, copy_row, freed_row, bw_GBps) / 2**30}
+            c_on.close()
+            result[part] = entry
+            print(f"[bench] policy {part}: full {entry['full']['ms_per_step']:.1f} ms, "
+                  f"plan {entry['plan']['ms_per_step']:.1f} ms", file=sys.stderr, flush=True)
+        result["all_resident_activation_GiB"] = S * freed_row / 2**30
+        result["kv_cache_GiB"] = B * S * 2 * Hkv * D * 2 / 2**30
+        return result
 
     print(f"[bench] workload={args.workload} steps={args.steps} warmup={args.warmup}", file=sys.stderr, flush=True)
     # Headline: exactly K timed steps, no per-kernel events in the stream.
@@ -288,6 +367,8 @@ def main():
             off["hidden_pct_vs_iso"] = 100.0 * max(0.0, min(1.0, 1.0 - off["exposed_ms_per_step"] / iso_ms))
         res["offload"] = off
         res["offload_hidden_pct"] = off.get("hidden_pct")
+        if offload == "qkvol" and not args.no_policy:
+            res["offload_policy"] = policy_compare(link["d2h_GBps"])
     ca.close()
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)

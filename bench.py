@@ -32,6 +32,7 @@ Reported (one JSON line):
   roofline       the dominant kernel (largest summed time), from HIP events
                  around every launch on the compute stream in K further timed
                  steps (kept out of the headline steps)
+  --sweep-n      replaces all of the above by one line per chunk count
   cpu_baseline   the fp64 oracle on a bounded sample (two heads, a prefix of
                  the sequence), in algorithmic TFLOP/s
 """
@@ -141,6 +142,41 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_bytes": nbytes, "copies": 3}), flush=True)
 
 
+def sweep_chunk_count(args, inp, S, Hq, Hkv, D, counts):
+    """Chunk-count trade-off on one GPU: for each N, the forward walk alone
+    and the full forward + backward walk (no offload), timed with events
+    over args.steps steps after args.warmup."""
+    import torch
+
+    from paper_2503_10377_amd.chunked import ChunkedAttention
+
+    st = torch.cuda.current_stream()
+    for n in counts:
+        ca = ChunkedAttention(1, S, n, Hq, Hkv, D, dtype="bf16", offload="none")
+        out = ca.alloc_outputs()
+        fl = algorithmic_flops(ca.offsets, 1, Hq, D)
+        row = {"sweep": "chunk_count", "seq_len": S, "n_chunks": n, "chunk_len": S // n, "n_q_heads": Hq,
+               "n_kv_heads": Hkv, "head_dim": D, "steps": args.steps}
+        for phase, run in (("fwd", lambda: ca.forward_only(inp, out)),
+                           ("fwd_bwd", lambda: ca.step(inp, out))):
+            for _ in range(args.warmup):
+                run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            for _ in range(args.steps):
+                run()
+            e1.record(st)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / args.steps
+            f = fl["fwd"] if phase == "fwd" else fl["total"]
+            row[f"{phase}_ms"] = ms
+            row[f"{phase}_tflops"] = f / (ms * 1e-3) / 1e12
+            row[f"{phase}_pct_peak"] = 100.0 * row[f"{phase}_tflops"] / PEAK_BF16_TFLOPS
+        ca.close()
+        print(json.dumps(row), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -155,6 +191,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-offload-compare", action="store_true")
     ap.add_argument("--no-policy", action="store_true", help="skip the partition / offload-ratio comparison")
+    ap.add_argument("--sweep-n", default="", metavar="N1,N2,...",
+                    help="instead of the headline line: one JSON line per chunk count N at the workload's S and "
+                         "heads, no offload (forward and forward+backward time and %% of peak)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -174,6 +213,9 @@ def main():
     B = 1
     torch.cuda.init()
     inp = make_inputs(B, S, Hq, Hkv, D, torch.bfloat16, seed=0, device="cuda")
+    if args.sweep_n:
+        sweep_chunk_count(args, inp, S, Hq, Hkv, D, [int(x) for x in args.sweep_n.split(",")])
+        return
     ca = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload=offload)
     out = ca.alloc_outputs()
     flops = algorithmic_flops(ca.offsets, B, Hq, D)

@@ -28,12 +28,13 @@ COMMON = [
     "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-function",
 ]
 
-# Per-source extra flags.  The forward keeps its MFMA accumulators in arch
-# VGPRs (the softmax reads S and rescales O with VALU ops, which would
-# otherwise shuttle them through AGPRs); it then fits 2 waves per SIMD.  The
-# backward kernels need more than 256 registers, so they keep the default.
+# Per-source extra flags.  The bf16 attention kernels keep their MFMA
+# results in arch VGPRs (the softmax reads S and dP with VALU ops, which would
+# otherwise copy them out of AGPRs one register at a time); the compiler then
+# places read-only MFMA operands (K/V or Q/dO fragments) in AGPRs.
 EXTRA = {
     "attn_fwd_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "attn_bwd_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

@@ -3,28 +3,36 @@
 // of SPPO) calls this for i = N-1..0; dK/dV accumulate across calls in fp32.
 //
 // Three kernels, all on the caller's stream:
-//   bwd_pre   Delta_r = <dO_r, O_r>                      (HBM-bound)
+//   bwd_pre   Delta_r = <dO_r, O_r> and LSE2_r = LSE_r * log2(e) into the
+//             context's workspace (HBM-bound)
 //   bwd_dkdv  one workgroup per 128 keys of one KV head (4 waves x 32 keys,
-//             lane <-> key); streams the chunk's query tiles (64 rows, every
-//             query head of the GQA group) through LDS (natural, swizzled
-//             layout; Q^T and dO^T operands by transposed reads) and accumulates
-//               dV += P^T dO,  dK += scale * dS^T Q
-//             in registers; S = Q K^T and dP = dO V^T are recomputed.
+//             lane <-> key, K/V fragments in registers); the chunk's query
+//             rows of every head of the GQA group stream through LDS in
+//             32-row sub-blocks, and per sub-block
+//               S = Q K^T, dP = dO V^T, P = exp2(S C - LSE2), dS = P (dP - Delta)
+//               dV += P^T dO,  dK += dS^T Q
 //   bwd_dq    one workgroup per 128 query rows of one head (lane <-> query);
-//             streams K/V tiles and accumulates dQ^T += K^T dS^T.
-// P = exp2(S*scale*log2e - LSE*log2e), dS = P (dP - Delta).
-#include <type_traits>
-
+//             keys stream through LDS in 32-key sub-blocks, and per sub-block
+//               S^T = K Q^T, dP^T = V dO^T, dS^T as above, dQ^T += K^T dS^T
+// Both stream their sub-blocks through a six-slot LDS ring by LDS-DMA, five
+// sub-blocks ahead, one barrier per sub-block, and software-pipeline them:
+// the MFMAs of sub-block n+1's S and dP run while the VALU forms sub-block
+// n's P and dS, then the gradient MFMAs of sub-block n run.  The order of
+// every step is fixed with sched_barrier, so operand reads sit a few MFMAs
+// ahead of their use.  Sub-blocks that need the causal mask are done one at
+// a time, outside the pipeline.
 #include "sppo_kernels.h"
 #include "tile_common.h"
 
 namespace sppo {
 namespace {
 
-constexpr int kDqBR = 128;    // query rows per dq workgroup
-constexpr int kDqBC = 64;     // keys per dq K/V tile
-constexpr int kKvBKV = 128;   // keys per dkdv workgroup
-constexpr int kKvBQ = 64;     // query rows per dkdv query tile
+constexpr int kKvKeys = 128;  // keys per dK/dV workgroup (4 waves x 32)
+constexpr int kDqRows = 128;  // query rows per dQ workgroup (4 waves x 32)
+constexpr int kSB = 32;       // rows (dK/dV) or keys (dQ) per sub-block
+constexpr int kRing = 6;      // LDS ring slots
+constexpr int kAhead = 5;     // sub-blocks loaded ahead of the one in use
+static_assert(kAhead == kRing - 1, "a slot is refilled right after its last reader");
 
 // ------------------------------------------------------------------ Delta
 template <int D>
@@ -50,221 +58,70 @@ __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(ChunkArgs a) {
     const int64_t h = item % a.Hq;
     const int64_t rr = (item / a.Hq) % s;
     const int64_t b = item / (a.Hq * s);
-    a.delta[(b * a.Hq + h) * s + rr] = acc;
-  }
-}
-
-// --------------------------------------------------------------------- dQ
-template <int D>
-__global__ __launch_bounds__(256) void bwd_dq_bf16_kernel(ChunkArgs a) {
-  constexpr int BR = kDqBR, BC = kDqBC;
-  using T = LdsTile<D>;
-  constexpr int NK = D / 16, ND = D / 32, CG = T::CG;
-  constexpr int ITEMS = (BC / 4) * CG;
-  constexpr int IPT = (ITEMS + 255) / 256;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BC * T::P];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[BC * T::P];
-
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int l32 = lane & 31, g = lane >> 5;
-  const int t = gridDim.x - 1 - blockIdx.x;
-  const int h = blockIdx.y;
-  const int64_t b = blockIdx.z;
-  const int hk = h / (a.Hq / a.Hkv);
-  const int64_t c0 = a.c0, c1 = a.c1, s = c1 - c0;
-  const int64_t q0 = c0 + (int64_t)t * BR;
-  const int64_t r = q0 + w * 32 + l32;
-  const bool rvalid = r < c1;
-  const int64_t kend = (q0 + BR < c1) ? q0 + BR : c1;
-  const int nkv = (int)((kend + BC - 1) / BC);
-  const float C = a.scale * kLog2e;
-  const auto nat = T::nat_base(lane);
-  const auto trb = T::tr_base(lane);
-
-  bf16x8 qf[NK], df[NK];
-  float lse2 = INFINITY, dl = 0.f;
-  if (rvalid) {
-    const int64_t off = ((b * s + (r - c0)) * a.Hq + h) * D;
-    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + off;
-    const uint16_t* drow = static_cast<const uint16_t*>(a.dout) + off;
-#pragma unroll
-    for (int kk = 0; kk < NK; ++kk) {
-      qf[kk] = as_bf16x8(ld_global16(qrow + 16 * kk + 8 * g));
-      df[kk] = as_bf16x8(ld_global16(drow + 16 * kk + 8 * g));
-    }
-    lse2 = a.lse[(b * a.Hq + h) * s + (r - c0)] * kLog2e;
-    dl = a.delta[(b * a.Hq + h) * s + (r - c0)];
-  } else {
-#pragma unroll
-    for (int kk = 0; kk < NK; ++kk) qf[kk] = df[kk] = bf16x8{};
-  }
-
-  const int64_t kvstride = (int64_t)a.Hkv * D;
-  const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + (b * a.S * a.Hkv + hk) * D;
-  const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + (b * a.S * a.Hkv + hk) * D;
-
-  f32x16 dq[ND];
-#pragma unroll
-  for (int db = 0; db < ND; ++db) dq[db] = f32x16{};
-
-  Block4x8 kreg[IPT], vreg[IPT];
-  Block4x8Offsets boff[IPT];
-#pragma unroll
-  for (int u = 0; u < IPT; ++u) {
-    const int c = tid + 256 * u;
-    boff[u] = block4x8_offsets(c / CG, c % CG, kvstride);
-  }
-  auto load_tile = [&](int it) {
-    const int64_t k0 = (int64_t)it * BC;
-    const auto rk = tile_rsrc(kbase + k0 * kvstride, c1 - k0, BC, kvstride);
-    const auto rv = tile_rsrc(vbase + k0 * kvstride, c1 - k0, BC, kvstride);
-#pragma unroll
-    for (int u = 0; u < IPT; ++u) {
-      if (ITEMS % 256 == 0 || tid + 256 * u < ITEMS) {
-        load_block4x8(kreg[u], rk, boff[u]);
-        load_block4x8(vreg[u], rv, boff[u]);
-      }
-    }
-  };
-
-  // One K/V tile as scheduling regions (see the dK/dV kernel):
-  //   1: natural K/V reads of keys 0..31
-  //   2: S^T, dP^T MFMAs of keys 0..31  + natural reads of keys 32..63
-  //   3: S^T, dP^T MFMAs of keys 32..63 + P, dS of keys 0..31 (VALU)
-  //                                     + transposed K reads for keys 0..31
-  //   4: dQ MFMAs over keys 0..31       + P, dS of keys 32..63
-  //   5: transposed K reads for keys 32..63, then their dQ MFMAs
-  auto tile_body = [&](int64_t k0, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    const int rel = (int)(r - k0);
-    f32x16 sv[2], dp[2];
-    bf16x8 dsb[4];
-    bf16x8 nk[NK], nv[NK];
-    bf16x8 tk[2][ND];
-
-    auto nat_reads = [&](int jb) {
-#pragma unroll
-      for (int kk = 0; kk < NK; ++kk) {
-        nk[kk] = ld_lds_nat<D>(Ks, nat, 32 * jb, kk);
-        nv[kk] = ld_lds_nat<D>(Vs, nat, 32 * jb, kk);
-      }
-    };
-    auto sdp_mfma = [&](int jb) {
-      sv[jb] = f32x16{};
-      dp[jb] = f32x16{};
-#pragma unroll
-      for (int kk = 0; kk < NK; ++kk) {
-        sv[jb] = mfma32(nk[kk], qf[kk], sv[jb]);
-        dp[jb] = mfma32(nv[kk], df[kk], dp[jb]);
-      }
-    };
-    auto softmax = [&](int jb) {
-      float ds[16];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float p = fast_exp2(sv[jb][v] * C - lse2);
-        if (MASK && 32 * jb + 8 * (v / 4) + 4 * g + (v % 4) > rel) p = 0.f;
-        ds[v] = p * (dp[jb][v] - dl);
-      }
-      dsb[2 * jb] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
-      dsb[2 * jb + 1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
-    };
-    auto tr_reads = [&](int jb) {
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-#pragma unroll
-        for (int db = 0; db < ND; ++db) tk[hh][db] = ld_lds_tr<D>(Ks, trb, 16 * (2 * jb + hh), 32 * db);
-      }
-    };
-    // dQ^T[d][query] += K^T dS^T: K^T comes from transposed reads of K.
-    auto dq_mfma = [&](int jb) {
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-#pragma unroll
-        for (int db = 0; db < ND; ++db) dq[db] = mfma32(tk[hh][db], dsb[2 * jb + hh], dq[db]);
-      }
-    };
-
-    nat_reads(0);
-    __builtin_amdgcn_sched_barrier(0);
-    sdp_mfma(0);
-    nat_reads(1);
-    __builtin_amdgcn_sched_barrier(0);
-    sdp_mfma(1);
-    softmax(0);
-    tr_reads(0);
-    __builtin_amdgcn_sched_barrier(0);
-    dq_mfma(0);
-    softmax(1);
-    __builtin_amdgcn_sched_barrier(0);
-    tr_reads(1);
-    __builtin_amdgcn_sched_barrier(0);
-    dq_mfma(1);
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
-  load_tile(0);
-  for (int it = 0; it < nkv; ++it) {
-    const int64_t k0 = (int64_t)it * BC;
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < IPT; ++u) {
-      const int c = tid + 256 * u;
-      if (ITEMS % 256 == 0 || c < ITEMS) {
-        const int rg = c / CG, cg = c % CG;
-        store_block_tile<D>(kreg[u], Ks, rg, cg);
-        store_block_tile<D>(vreg[u], Vs, rg, cg);
-      }
-    }
-    __syncthreads();
-    load_tile(it + 1 < nkv ? it + 1 : it);  // the last prefetch repeats a tile, harmlessly
-
-    if (k0 + BC - 1 > q0 + 32 * w) {
-      tile_body(k0, std::true_type{});
-    } else {
-      tile_body(k0, std::false_type{});
-    }
-  }
-
-  if (rvalid) {
-    uint16_t* qrow = static_cast<uint16_t*>(a.dq) + ((b * s + (r - c0)) * a.Hq + h) * D;
-#pragma unroll
-    for (int db = 0; db < ND; ++db) {
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        *reinterpret_cast<u32x2*>(qrow + 32 * db + 8 * q4 + 4 * g) =
-            pack_bf16x4(dq[db][4 * q4 + 0] * a.scale, dq[db][4 * q4 + 1] * a.scale,
-                        dq[db][4 * q4 + 2] * a.scale, dq[db][4 * q4 + 3] * a.scale);
-      }
-    }
+    const int64_t idx = (b * a.Hq + h) * s + rr;
+    a.delta[idx] = acc;
+    a.lse2[idx] = a.lse[idx] * kLog2e;
   }
 }
 
 // ------------------------------------------------------------------ dK dV
 template <int D>
-__global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
-  constexpr int BQ = kKvBQ;
-  using T = LdsTile<D>;
-  constexpr int NK = D / 16, ND = D / 32, CG = T::CG;
-  constexpr int ITEMS = (BQ / 4) * CG;
-  constexpr int IPT = (ITEMS + 255) / 256;
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[BQ * T::P];
-  __shared__ __attribute__((aligned(16))) uint16_t Ds[BQ * T::P];
-  __shared__ __attribute__((aligned(16))) float lse2s[BQ];
-  __shared__ __attribute__((aligned(16))) float dls[BQ];
+__global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
+  using T = XTile<D>;
+  constexpr int P = T::P, NK = D / 16, ND = D / 32;
+  constexpr int IPWQ = (kSB / T::RPI) / 4;  // DMA instructions per wave per tensor per sub-block
+  static_assert(IPWQ >= 1 && IPWQ * 4 * T::RPI == kSB, "sub-block splits over 4 waves");
+  constexpr int DMA_PER_SB = 2 * IPWQ + 1;  // Q, dO, and one for the [LSE2 | Delta] record
+  // One LDS object per ring slot: [Q rows | dO rows | LSE2 (32 floats) | Delta (32 floats)].
+  constexpr int SLOT = 2 * kSB * P + 128;
+  __shared__ __attribute__((aligned(1024))) uint16_t R0[SLOT], R1[SLOT], R2[SLOT], R3[SLOT], R4[SLOT], R5[SLOT];
+  auto slot = [&](auto I) -> uint16_t* {
+    constexpr int i = decltype(I)::value;
+    if constexpr (i == 0) return R0; else if constexpr (i == 1) return R1; else if constexpr (i == 2) return R2;
+    else if constexpr (i == 3) return R3; else if constexpr (i == 4) return R4; else return R5;
+  };
+  auto qbuf = [&](auto I) -> uint16_t* { return slot(I); };
+  auto obuf = [&](auto I) -> uint16_t* { return slot(I) + kSB * P; };
+  auto lbuf = [&](auto I) -> float* { return reinterpret_cast<float*>(slot(I) + 2 * kSB * P); };
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, g = lane >> 5;
   const int hk = blockIdx.y;
   const int64_t b = blockIdx.z;
   const int G = a.Hq / a.Hkv;
   const int64_t c0 = a.c0, c1 = a.c1, s = c1 - c0;
   const int64_t kv1 = a.kv1;
-  const int64_t k0 = a.kv0 + (int64_t)blockIdx.x * kKvBKV;
+  const int64_t k0 = a.kv0 + (int64_t)blockIdx.x * kKvKeys;
   const int64_t j = k0 + 32 * w + l32;  // this lane's key
   const float C = a.scale * kLog2e;
-  const auto nat = T::nat_base(lane);
-  const auto trb = T::tr_base(lane);
+
+  // Query sub-blocks (chunk-local, 32 rows from c0): [sb_begin, sb_u) need
+  // the mask, [sb_u, nsb) see every key of the workgroup.
+  const int nsb = (int)((s + kSB - 1) / kSB);
+  const int sb_begin = k0 > c0 ? (int)((k0 - c0) / kSB) : 0;
+  int sb_u = (int)((k0 + kKvKeys - c0 + kSB - 1) / kSB);
+  if (sb_u > nsb) sb_u = nsb;
+  if (sb_u < sb_begin) sb_u = sb_begin;
+  const int N = nsb - sb_u;  // unmasked sub-blocks per head
+
+  int nat[NK];
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk) nat[kk] = T::nat(lane, kk);
+  int tro[ND][2];
+#pragma unroll
+  for (int db = 0; db < ND; ++db) {
+    tro[db][0] = T::tr(lane, db, 0);
+    tro[db][1] = T::tr(lane, db, 1);
+  }
+  const int64_t qstride = (int64_t)a.Hq * D;
+  int dmaq[IPWQ];
+#pragma unroll
+  for (int x = 0; x < IPWQ; ++x) dmaq[x] = T::dma(lane, w * IPWQ + x, qstride);
+  // The [LSE2 | Delta] record: waves 0, 1 load LSE2 rows 0..15, 16..31, waves
+  // 2, 3 Delta, 16 lanes each.
+  const int dmal = (16 * (w & 1) + (lane & 15)) * 4;
+  const float* lsrc = (w < 2) ? a.lse2 : a.delta;
+  const int ldst = 32 * (w >> 1) + 16 * (w & 1);
 
   bf16x8 kf[NK], vf[NK];
   {
@@ -277,173 +134,203 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
       vf[kk] = j < kv1 ? as_bf16x8(ld_global16(vrow + 16 * kk + 8 * g)) : bf16x8{};
     }
   }
-
   f32x16 dk[ND], dv[ND];
 #pragma unroll
   for (int db = 0; db < ND; ++db) dk[db] = dv[db] = f32x16{};
 
-  // Query tiles (chunk-local) that can see a key of this workgroup.
-  const int64_t qt_begin = k0 > c0 ? (k0 - c0) / BQ : 0;
-  const int64_t nqt = (s + BQ - 1) / BQ;
-
-  const int64_t qstride = (int64_t)a.Hq * D;
-  Block4x8 qreg[IPT], dreg[IPT];
-  Block4x8Offsets boff[IPT];
+  // DMA of query sub-block sb of head h into a slot; rows past the chunk load
+  // zeros, so every call issues DMA_PER_SB instructions per wave.
+  auto issue = [&](int h, int sb, uint16_t* qd, uint16_t* od, float* ld) {
+    const int64_t r0 = (int64_t)sb * kSB;
+    const int64_t valid = s - r0;
+    const int64_t tile0 = (b * s + r0) * a.Hq + h;
+    const auto rq = tile_rsrc(static_cast<const uint16_t*>(a.q) + tile0 * D, valid, kSB, qstride);
+    const auto ro = tile_rsrc(static_cast<const uint16_t*>(a.dout) + tile0 * D, valid, kSB, qstride);
 #pragma unroll
-  for (int u = 0; u < IPT; ++u) {
-    const int c = tid + 256 * u;
-    boff[u] = block4x8_offsets(c / CG, c % CG, qstride);
-  }
-  float lse_r = INFINITY, dl_r = 0.f;
-  auto load_tile = [&](int h, int64_t qt) {
-    const int64_t tile0 = (b * s + qt * BQ) * a.Hq + h;  // first row of the tile, in D-element units
-    const auto rq = tile_rsrc(static_cast<const uint16_t*>(a.q) + tile0 * D, s - qt * BQ, BQ, qstride);
-    const auto rd = tile_rsrc(static_cast<const uint16_t*>(a.dout) + tile0 * D, s - qt * BQ, BQ, qstride);
-#pragma unroll
-    for (int u = 0; u < IPT; ++u) {
-      if (ITEMS % 256 == 0 || tid + 256 * u < ITEMS) {
-        load_block4x8(qreg[u], rq, boff[u]);
-        load_block4x8(dreg[u], rd, boff[u]);
-      }
+    for (int x = 0; x < IPWQ; ++x) {
+      lds_dma16(rq, qd + (w * IPWQ + x) * 512, dmaq[x]);
+      lds_dma16(ro, od + (w * IPWQ + x) * 512, dmaq[x]);
     }
-    if (tid < BQ) {
-      const int64_t rr = qt * BQ + tid;
-      lse_r = rr < s ? a.lse[(b * a.Hq + h) * s + rr] * kLog2e : INFINITY;
-      dl_r = rr < s ? a.delta[(b * a.Hq + h) * s + rr] : 0.f;
+    const int64_t nrec = valid <= 0 ? 0 : (valid < kSB ? valid : kSB);
+    const uint64_t lb = reinterpret_cast<uint64_t>(lsrc + (b * a.Hq + h) * s + r0);
+    const uint64_t lbu = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(lb >> 32)) << 32) |
+                         (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)lb);
+    const auto rl = __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<float*>(lbu), (short)0,
+                                                      __builtin_amdgcn_readfirstlane((int)(nrec * 4)), kBufferFlags);
+    if (lane < 16) lds_dma4(rl, ld + ldst, dmal);
+  };
+  // Stream position n of head h -> sub-block sb_u + n; past the stream: zeros.
+  auto stream_issue = [&](int h, int n, uint16_t* qd, uint16_t* od, float* ld) {
+    issue(h, n < N ? sb_u + n : nsb, qd, od, ld);
+  };
+  auto tr_rd = [&](const uint16_t* X, int hh, int db) {
+    return ld_tr(X, tro[db][0] + 16 * hh * P, tro[db][1] + 16 * hh * P);
+  };
+  // S = Q K^T and dP = dO V^T of one sub-block (lane <-> key).
+  auto sdp = [&](const uint16_t* Qs, const uint16_t* Os, f32x16& sv, f32x16& dp) {
+    sv = mfma32(ld_nat(Qs, nat[0]), kf[0], f32x16{});
+    dp = mfma32(ld_nat(Os, nat[0]), vf[0], f32x16{});
+#pragma unroll
+    for (int kk = 1; kk < NK; ++kk) {
+      sv = mfma32(ld_nat(Qs, nat[kk]), kf[kk], sv);
+      dp = mfma32(ld_nat(Os, nat[kk]), vf[kk], dp);
     }
   };
-
-  // One query tile, as five scheduling regions (sched_barrier between them
-  // keeps the compiler from sinking LDS reads next to their MFMAs):
-  //   1: natural reads of Q/dO rows 0..31
-  //   2: S, dP MFMAs of rows 0..31        + natural reads of rows 32..63
-  //   3: S, dP MFMAs of rows 32..63       + P, dS of rows 0..31 (VALU)
-  //                                       + transposed Q/dO reads for rows 0..31
-  //   4: dV, dK MFMAs of rows 0..31       + P, dS of rows 32..63
-  //   5: transposed reads for rows 32..63, then their dV, dK MFMAs
-  // so every MFMA batch has its operands in flight one region ahead and the
-  // softmax VALU work of one row block can overlap the MFMAs of the other.
-  // MASK selects the diagonal variant.
-  auto tile_body = [&](int64_t q0, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    const int rel = (int)(j - q0);  // this lane's key relative to the query tile
-    f32x16 sv[2], dp[2];
-    bf16x8 pb[2][2], dsb[2][2];
-    bf16x8 nq[NK], nd[NK];
-    bf16x8 tq[2][ND], td[2][ND];
-
-    auto nat_reads = [&](int ib) {
+  // dV += P^T dO, dK += dS^T Q of one sub-block.
+  auto grads = [&](const uint16_t* Qs, const uint16_t* Os, const bf16x8 (&pb)[2], const bf16x8 (&dsb)[2]) {
 #pragma unroll
-      for (int kk = 0; kk < NK; ++kk) {
-        nq[kk] = ld_lds_nat<D>(Qs, nat, 32 * ib, kk);
-        nd[kk] = ld_lds_nat<D>(Ds, nat, 32 * ib, kk);
-      }
-    };
-    auto sdp_mfma = [&](int ib) {
-      sv[ib] = f32x16{};
-      dp[ib] = f32x16{};
-#pragma unroll
-      for (int kk = 0; kk < NK; ++kk) {
-        sv[ib] = mfma32(nq[kk], kf[kk], sv[ib]);
-        dp[ib] = mfma32(nd[kk], vf[kk], dp[ib]);
-      }
-    };
-    auto softmax = [&](int ib) {
-      float p[16], ds[16];
-#pragma unroll
-      for (int v4 = 0; v4 < 4; ++v4) {
-        const int qi = 32 * ib + 8 * v4 + 4 * g;
-        const float4 l4 = *reinterpret_cast<const float4*>(lse2s + qi);
-        const float4 d4 = *reinterpret_cast<const float4*>(dls + qi);
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-        const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int v = 4 * v4 + e;
-          float pv = fast_exp2(sv[ib][v] * C - lv[e]);
-          if (MASK && rel > qi + e) pv = 0.f;
-          p[v] = pv;
-          ds[v] = pv * (dp[ib][v] - dv4[e]);
-        }
-      }
-      pb[ib][0] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
-      pb[ib][1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
-      dsb[ib][0] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
-      dsb[ib][1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
-    };
-    auto tr_reads = [&](int ib, int hh) {
+    for (int hh = 0; hh < 2; ++hh) {
 #pragma unroll
       for (int db = 0; db < ND; ++db) {
-        tq[hh][db] = ld_lds_tr<D>(Qs, trb, 16 * (2 * ib + hh), 32 * db);
-        td[hh][db] = ld_lds_tr<D>(Ds, trb, 16 * (2 * ib + hh), 32 * db);
-      }
-    };
-    auto dkdv_mfma = [&](int ib) {
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-#pragma unroll
-        for (int db = 0; db < ND; ++db) {
-          dv[db] = mfma32(pb[ib][hh], td[hh][db], dv[db]);
-          dk[db] = mfma32(dsb[ib][hh], tq[hh][db], dk[db]);
-        }
-      }
-    };
-
-    nat_reads(0);
-    __builtin_amdgcn_sched_barrier(0);
-    sdp_mfma(0);
-    nat_reads(1);
-    __builtin_amdgcn_sched_barrier(0);
-    sdp_mfma(1);
-    softmax(0);
-    tr_reads(0, 0);
-    tr_reads(0, 1);
-    __builtin_amdgcn_sched_barrier(0);
-    dkdv_mfma(0);
-    softmax(1);
-    __builtin_amdgcn_sched_barrier(0);
-    tr_reads(1, 0);
-    tr_reads(1, 1);
-    __builtin_amdgcn_sched_barrier(0);
-    dkdv_mfma(1);
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
-  load_tile(hk * G, qt_begin);
-  for (int hh = 0; hh < G; ++hh) {
-    for (int64_t qt = qt_begin; qt < nqt; ++qt) {
-      __syncthreads();
-#pragma unroll
-      for (int u = 0; u < IPT; ++u) {
-        const int c = tid + 256 * u;
-        if (ITEMS % 256 == 0 || c < ITEMS) {
-          const int rg = c / CG, cg = c % CG;
-          store_block_tile<D>(qreg[u], Qs, rg, cg);
-          store_block_tile<D>(dreg[u], Ds, rg, cg);
-        }
-      }
-      if (tid < BQ) {
-        lse2s[tid] = lse_r;
-        dls[tid] = dl_r;
-      }
-      __syncthreads();
-      // Prefetch the next tile (the same one again after the last, harmless).
-      {
-        int nh = hh;
-        int64_t nq = qt + 1;
-        if (nq == nqt) {
-          nq = qt_begin;
-          nh = hh + 1 < G ? hh + 1 : hh;
-        }
-        load_tile(hk * G + nh, nq);
-      }
-      const int64_t q0 = c0 + qt * BQ;
-      if (k0 + 32 * w + 31 > q0) {
-        tile_body(q0, std::true_type{});
-      } else {
-        tile_body(q0, std::false_type{});
+        dv[db] = mfma32(pb[hh], tr_rd(Os, hh, db), dv[db]);
+        dk[db] = mfma32(dsb[hh], tr_rd(Qs, hh, db), dk[db]);
       }
     }
+  };
+
+  // Heads of the GQA group one after another, each in row order: the masked
+  // sub-blocks one at a time, then the unmasked stream.  A key's dK/dV thus
+  // sums its rows in the same order whatever range of keys a launch covers
+  // (rows before a key add exact zeros).
+  for (int hh = 0; hh < G; ++hh) {
+    const int h = hk * G + hh;
+    // ---- sub-blocks with the causal mask, one at a time (slot 0)
+    for (int sb = sb_begin; sb < sb_u; ++sb) {
+      __syncthreads();
+      issue(h, sb, qbuf(IC<0>{}), obuf(IC<0>{}), lbuf(IC<0>{}));
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+      __syncthreads();
+      f32x16 sv, dp;
+      sdp(qbuf(IC<0>{}), obuf(IC<0>{}), sv, dp);
+      const float* ld = lbuf(IC<0>{});
+      const int64_t r0g = c0 + (int64_t)sb * kSB;  // global row of the sub-block's first row
+      float p[16], ds[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int qi = 8 * (v / 4) + 4 * g + (v % 4);
+        float pv = fast_exp2(sv[v] * C - ld[qi]);
+        if (j > r0g + qi) pv = 0.f;  // key j sees row r iff j <= r
+        p[v] = pv;
+        ds[v] = pv * (dp[v] - ld[32 + qi]);
+      }
+      bf16x8 pb[2], dsb[2];
+      pb[0] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+      pb[1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
+      dsb[0] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
+      dsb[1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
+      grads(qbuf(IC<0>{}), obuf(IC<0>{}), pb, dsb);
+    }
+
+    // ---- unmasked stream, software pipelined
+    if (N == 0) continue;
+    __syncthreads();  // every slot is free
+    stream_issue(h, 0, qbuf(IC<0>{}), obuf(IC<0>{}), lbuf(IC<0>{}));
+    stream_issue(h, 1, qbuf(IC<1>{}), obuf(IC<1>{}), lbuf(IC<1>{}));
+    stream_issue(h, 2, qbuf(IC<2>{}), obuf(IC<2>{}), lbuf(IC<2>{}));
+    stream_issue(h, 3, qbuf(IC<3>{}), obuf(IC<3>{}), lbuf(IC<3>{}));
+    stream_issue(h, 4, qbuf(IC<4>{}), obuf(IC<4>{}), lbuf(IC<4>{}));
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - 1) * DMA_PER_SB));
+    __syncthreads();
+    f32x16 sa, da, sb2, db2;
+    sdp(qbuf(IC<0>{}), obuf(IC<0>{}), sa, da);
+    // Step n in slot I: A(n) reads slot I+1 (natural) and slot I's record;
+    // B(n) reads slot I (transposed).  At its start sub-block n+1 has landed
+    // (only sub-blocks n+2..n+4 may still be loading); then sub-block n+5
+    // goes to slot I+5 = I-1, free since step n-1.
+    auto step = [&](int n, auto sl, f32x16& scur, f32x16& dcur, f32x16& snext, f32x16& dnext) {
+      constexpr int I = decltype(sl)::value;
+      constexpr int I1 = (I + 1) % kRing, I5 = (I + kAhead) % kRing;
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - 2) * DMA_PER_SB));
+      __syncthreads();
+      stream_issue(h, n + kAhead, qbuf(IC<I5>{}), obuf(IC<I5>{}), lbuf(IC<I5>{}));
+      const uint16_t* Qn = qbuf(IC<I1>{});
+      const uint16_t* On = obuf(IC<I1>{});
+      const uint16_t* Qc = qbuf(IC<I>{});
+      const uint16_t* Oc = obuf(IC<I>{});
+      const float* ld = lbuf(IC<I>{});
+      // A(n): MFMA m (NA of them) is S(n+1) (m even) or dP(n+1) (m odd),
+      // k-step m/2; its operand is read four MFMAs ahead.  The VALU turns the
+      // 16 elements of S(n), dP(n) into P(n), dS(n), element i beside MFMA
+      // i / (16 / NA).
+      constexpr int NA = 2 * NK, EPM = 16 / NA;
+      auto nat_op = [&](int m) { return ld_nat((m & 1) ? On : Qn, nat[m >> 1]); };
+      bf16x8 op[NA];
+      op[0] = nat_op(0);
+      op[1] = nat_op(1);
+      op[2] = nat_op(2);
+      op[3] = nat_op(3);
+      float4 l4 = *reinterpret_cast<const float4*>(ld + 4 * g);
+      float4 d4 = *reinterpret_cast<const float4*>(ld + 32 + 4 * g);
+      float p[16], ds[16];
+      bf16x8 pb[2], dsb[2];
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        if (i % EPM == 0) {
+          const int mi = i / EPM;
+          if (mi & 1) {
+            dnext = mfma32(op[mi], vf[mi >> 1], mi == 1 ? f32x16{} : dnext);
+          } else {
+            snext = mfma32(op[mi], kf[mi >> 1], mi == 0 ? f32x16{} : snext);
+          }
+          if (mi + 4 < NA) op[mi + 4] = nat_op(mi + 4);
+        }
+        const int e = i & 3;
+        const float lv = e == 0 ? l4.x : e == 1 ? l4.y : e == 2 ? l4.z : l4.w;
+        const float dl = e == 0 ? d4.x : e == 1 ? d4.y : e == 2 ? d4.z : d4.w;
+        p[i] = fast_exp2(scur[i] * C - lv);
+        ds[i] = p[i] * (dcur[i] - dl);
+        if (e == 3 && i < 15) {  // rows 8 (v/4) + 4 g + v%4 of the next group of four
+          l4 = *reinterpret_cast<const float4*>(ld + 8 * ((i + 1) >> 2) + 4 * g);
+          d4 = *reinterpret_cast<const float4*>(ld + 32 + 8 * ((i + 1) >> 2) + 4 * g);
+        }
+        if ((i & 7) == 7) {
+          const int h8 = i >> 3, q = 8 * h8;
+          pb[h8] = pack_bf16x8(p[q], p[q + 1], p[q + 2], p[q + 3], p[q + 4], p[q + 5], p[q + 6], p[q + 7]);
+          dsb[h8] = pack_bf16x8(ds[q], ds[q + 1], ds[q + 2], ds[q + 3], ds[q + 4], ds[q + 5], ds[q + 6], ds[q + 7]);
+        }
+        if (i % EPM == EPM - 1) __builtin_amdgcn_sched_barrier(0);
+      }
+      // B(n): MFMA jj is dV (jj even) or dK (jj odd) for k-half hh, d-block
+      // db; its transposed operand is read three slots ahead.
+      constexpr int NB = 4 * ND;
+      auto tr_op = [&](int jj) {
+        const int blk = jj >> 1;
+        return tr_rd((jj & 1) ? Qc : Oc, blk / ND, blk % ND);
+      };
+      bf16x8 top[NB];
+      top[0] = tr_op(0);
+      top[1] = tr_op(1);
+      top[2] = tr_op(2);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int jj = 0; jj < NB; ++jj) {
+        const int blk = jj >> 1, hh = blk / ND, db = blk % ND;
+        if (jj & 1) {
+          dk[db] = mfma32(dsb[hh], top[jj], dk[db]);
+        } else {
+          dv[db] = mfma32(pb[hh], top[jj], dv[db]);
+        }
+        if (jj + 3 < NB) top[jj + 3] = tr_op(jj + 3);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    // Past the last sub-block A still computes S, dP of the (zero) next slot;
+    // they are never used.
+    for (int n = 0; n < N; n += kRing) {
+      step(n, IC<0>{}, sa, da, sb2, db2);
+      if (n + 1 >= N) break;
+      step(n + 1, IC<1>{}, sb2, db2, sa, da);
+      if (n + 2 >= N) break;
+      step(n + 2, IC<2>{}, sa, da, sb2, db2);
+      if (n + 3 >= N) break;
+      step(n + 3, IC<3>{}, sb2, db2, sa, da);
+      if (n + 4 >= N) break;
+      step(n + 4, IC<4>{}, sa, da, sb2, db2);
+      if (n + 5 >= N) break;
+      step(n + 5, IC<5>{}, sb2, db2, sa, da);
+    }
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no LDS-DMA in flight past the stream
   }
 
   // Write back rows [k0, k0+128) n [kv0, kv1): lane <-> d, v <-> key.
@@ -468,6 +355,234 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   }
 }
 
+// --------------------------------------------------------------------- dQ
+template <int D>
+__global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
+  using T = XTile<D>;
+  constexpr int P = T::P, NK = D / 16, ND = D / 32;
+  constexpr int IPWK = (kSB / T::RPI) / 4;  // DMA instructions per wave per tensor per sub-block
+  static_assert(IPWK >= 1 && IPWK * 4 * T::RPI == kSB, "sub-block splits over 4 waves");
+  constexpr int DMA_PER_SB = 2 * IPWK;
+  // One LDS object per ring slot: [K rows | V rows].
+  constexpr int SLOT = 2 * kSB * P;
+  __shared__ __attribute__((aligned(1024))) uint16_t R0[SLOT], R1[SLOT], R2[SLOT], R3[SLOT], R4[SLOT], R5[SLOT];
+  auto slot = [&](auto I) -> uint16_t* {
+    constexpr int i = decltype(I)::value;
+    if constexpr (i == 0) return R0; else if constexpr (i == 1) return R1; else if constexpr (i == 2) return R2;
+    else if constexpr (i == 3) return R3; else if constexpr (i == 4) return R4; else return R5;
+  };
+  auto slot_rt = [&](int i) -> uint16_t* {
+    return i == 0 ? R0 : i == 1 ? R1 : i == 2 ? R2 : i == 3 ? R3 : i == 4 ? R4 : R5;
+  };
+
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, g = lane >> 5;
+  const int t = gridDim.x - 1 - blockIdx.x;  // longest (latest) query tiles first
+  const int h = blockIdx.y;
+  const int64_t b = blockIdx.z;
+  const int hk = h / (a.Hq / a.Hkv);
+  const int64_t c0 = a.c0, c1 = a.c1, s = c1 - c0;
+  const int64_t q0 = c0 + (int64_t)t * kDqRows;
+  const int64_t r = q0 + 32 * w + l32;
+  const bool rvalid = r < c1;
+  const int64_t kend = (q0 + kDqRows < c1) ? q0 + kDqRows : c1;
+  const int nsub = (int)((kend + kSB - 1) / kSB);
+  const int N = (int)(q0 / kSB);  // key sub-blocks every row of the workgroup sees in full
+  const float C = a.scale * kLog2e;
+
+  int nat[NK];
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk) nat[kk] = T::nat(lane, kk);
+  int tro[ND][2];
+#pragma unroll
+  for (int db = 0; db < ND; ++db) {
+    tro[db][0] = T::tr(lane, db, 0);
+    tro[db][1] = T::tr(lane, db, 1);
+  }
+  const int64_t kvstride = (int64_t)a.Hkv * D;
+  int dmak[IPWK];
+#pragma unroll
+  for (int x = 0; x < IPWK; ++x) dmak[x] = T::dma(lane, w * IPWK + x, kvstride);
+  const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + (b * a.S * a.Hkv + hk) * D;
+  const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + (b * a.S * a.Hkv + hk) * D;
+
+  bf16x8 qf[NK], df[NK];
+  float lse2 = INFINITY, dl = 0.f;  // a padding row gets P = 0
+  if (rvalid) {
+    const int64_t off = ((b * s + (r - c0)) * a.Hq + h) * D;
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + off;
+    const uint16_t* drow = static_cast<const uint16_t*>(a.dout) + off;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      qf[kk] = as_bf16x8(ld_global16(qrow + 16 * kk + 8 * g));
+      df[kk] = as_bf16x8(ld_global16(drow + 16 * kk + 8 * g));
+    }
+    lse2 = a.lse2[(b * a.Hq + h) * s + (r - c0)];
+    dl = a.delta[(b * a.Hq + h) * s + (r - c0)];
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) qf[kk] = df[kk] = bf16x8{};
+  }
+  f32x16 dq[ND];
+#pragma unroll
+  for (int db = 0; db < ND; ++db) dq[db] = f32x16{};
+
+  // DMA of K/V sub-block u (keys [32u, 32u+32)) into a slot; keys past the
+  // chunk end load zeros, so every call issues DMA_PER_SB instructions.
+  auto issue = [&](int u, uint16_t* dst) {
+    const int64_t k0 = (int64_t)u * kSB;
+    const auto rk = tile_rsrc(kbase + k0 * kvstride, c1 - k0, kSB, kvstride);
+    const auto rv = tile_rsrc(vbase + k0 * kvstride, c1 - k0, kSB, kvstride);
+#pragma unroll
+    for (int x = 0; x < IPWK; ++x) {
+      lds_dma16(rk, dst + (w * IPWK + x) * 512, dmak[x]);
+      lds_dma16(rv, dst + kSB * P + (w * IPWK + x) * 512, dmak[x]);
+    }
+  };
+  auto tr_rd = [&](const uint16_t* X, int hh, int db) {
+    return ld_tr(X, tro[db][0] + 16 * hh * P, tro[db][1] + 16 * hh * P);
+  };
+  // S^T = K Q^T and dP^T = V dO^T of one sub-block (lane <-> query).
+  auto sdp = [&](const uint16_t* K, f32x16& sv, f32x16& dp) {
+    const uint16_t* V = K + kSB * P;
+    sv = mfma32(ld_nat(K, nat[0]), qf[0], f32x16{});
+    dp = mfma32(ld_nat(V, nat[0]), df[0], f32x16{});
+#pragma unroll
+    for (int kk = 1; kk < NK; ++kk) {
+      sv = mfma32(ld_nat(K, nat[kk]), qf[kk], sv);
+      dp = mfma32(ld_nat(V, nat[kk]), df[kk], dp);
+    }
+  };
+
+  // Prologue: sub-blocks 0..4 (which also covers every diagonal sub-block
+  // when N is 0).
+  issue(0, R0);
+  issue(1, R1);
+  issue(2, R2);
+  issue(3, R3);
+  issue(4, R4);
+
+  if (N > 0) {
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - 1) * DMA_PER_SB));
+    __syncthreads();
+    f32x16 sa, da, sb2, db2;
+    sdp(R0, sa, da);
+    // Step n in slot I: A(n) reads slot I+1 (natural K, V); B(n) reads slot I
+    // (transposed K).  At its start sub-block n+1 has landed; then sub-block
+    // n+5 goes to slot I+5 = I-1, free since step n-1.
+    auto step = [&](int n, auto sl, f32x16& scur, f32x16& dcur, f32x16& snext, f32x16& dnext) {
+      constexpr int I = decltype(sl)::value;
+      constexpr int I1 = (I + 1) % kRing, I5 = (I + kAhead) % kRing;
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - 2) * DMA_PER_SB));
+      __syncthreads();
+      issue(n + kAhead, slot(IC<I5>{}));
+      const uint16_t* Kn = slot(IC<I1>{});
+      const uint16_t* Vn = Kn + kSB * P;
+      const uint16_t* Kc = slot(IC<I>{});
+      // A(n): MFMA m (NA of them) is S^T(n+1) (m even) or dP^T(n+1) (m odd),
+      // k-step m/2; its operand is read four MFMAs ahead.  The VALU turns the
+      // 16 elements of S^T(n), dP^T(n) into dS^T(n), element i beside MFMA
+      // i / (16 / NA).
+      constexpr int NA = 2 * NK, EPM = 16 / NA;
+      auto nat_op = [&](int m) { return ld_nat((m & 1) ? Vn : Kn, nat[m >> 1]); };
+      bf16x8 op[NA];
+      op[0] = nat_op(0);
+      op[1] = nat_op(1);
+      op[2] = nat_op(2);
+      op[3] = nat_op(3);
+      float ds[16];
+      bf16x8 dsb[2];
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        if (i % EPM == 0) {
+          const int mi = i / EPM;
+          if (mi & 1) {
+            dnext = mfma32(op[mi], df[mi >> 1], mi == 1 ? f32x16{} : dnext);
+          } else {
+            snext = mfma32(op[mi], qf[mi >> 1], mi == 0 ? f32x16{} : snext);
+          }
+          if (mi + 4 < NA) op[mi + 4] = nat_op(mi + 4);
+        }
+        const float p = fast_exp2(scur[i] * C - lse2);
+        ds[i] = p * (dcur[i] - dl);
+        if ((i & 7) == 7) {
+          const int h8 = i >> 3, q = 8 * h8;
+          dsb[h8] = pack_bf16x8(ds[q], ds[q + 1], ds[q + 2], ds[q + 3], ds[q + 4], ds[q + 5], ds[q + 6], ds[q + 7]);
+        }
+        if (i % EPM == EPM - 1) __builtin_amdgcn_sched_barrier(0);
+      }
+      // B(n): MFMA jj is dQ^T d-block jj % ND for k-half jj / ND; its
+      // transposed K operand is read three slots ahead.
+      constexpr int NB = 2 * ND;
+      auto tr_op = [&](int jj) { return tr_rd(Kc, jj / ND, jj % ND); };
+      bf16x8 top[NB];
+      top[0] = tr_op(0);
+      top[1] = tr_op(1);
+      top[2] = tr_op(2);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int jj = 0; jj < NB; ++jj) {
+        dq[jj % ND] = mfma32(top[jj], dsb[jj / ND], dq[jj % ND]);
+        if (jj + 3 < NB) top[jj + 3] = tr_op(jj + 3);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    for (int n = 0; n < N; n += kRing) {
+      step(n, IC<0>{}, sa, da, sb2, db2);
+      if (n + 1 >= N) break;
+      step(n + 1, IC<1>{}, sb2, db2, sa, da);
+      if (n + 2 >= N) break;
+      step(n + 2, IC<2>{}, sa, da, sb2, db2);
+      if (n + 3 >= N) break;
+      step(n + 3, IC<3>{}, sb2, db2, sa, da);
+      if (n + 4 >= N) break;
+      step(n + 4, IC<4>{}, sa, da, sb2, db2);
+      if (n + 5 >= N) break;
+      step(n + 5, IC<5>{}, sb2, db2, sa, da);
+    }
+  }
+
+  // Diagonal sub-blocks [N, nsub) (at most five): already in the ring, since
+  // the steady loop loaded five ahead and the prologue covers N = 0.
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  __syncthreads();
+  for (int u = N; u < nsub; ++u) {
+    const uint16_t* K = slot_rt(u % kRing);
+    f32x16 sv, dp;
+    sdp(K, sv, dp);
+    const int rel = (int)(r - (int64_t)u * kSB);  // keys past this row are masked
+    float ds[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float p = fast_exp2(sv[v] * C - lse2);
+      if (8 * (v / 4) + 4 * g + (v % 4) > rel) p = 0.f;
+      ds[v] = p * (dp[v] - dl);
+    }
+    bf16x8 dsb[2];
+    dsb[0] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
+    dsb[1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+      for (int db = 0; db < ND; ++db) dq[db] = mfma32(tr_rd(K, hh, db), dsb[hh], dq[db]);
+    }
+  }
+
+  if (rvalid) {
+    uint16_t* qrow = static_cast<uint16_t*>(a.dq) + ((b * s + (r - c0)) * a.Hq + h) * D;
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        *reinterpret_cast<u32x2*>(qrow + 32 * db + 8 * q4 + 4 * g) =
+            pack_bf16x4(dq[db][4 * q4 + 0] * a.scale, dq[db][4 * q4 + 1] * a.scale,
+                        dq[db][4 * q4 + 2] * a.scale, dq[db][4 * q4 + 3] * a.scale);
+      }
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_bwd_pre_bf16(const ChunkArgs& a, hipStream_t stream) {
@@ -486,7 +601,7 @@ hipError_t launch_bwd_pre_bf16(const ChunkArgs& a, hipStream_t stream) {
 
 hipError_t launch_bwd_dkdv_bf16(const ChunkArgs& a, hipStream_t stream) {
   if (a.kv0 < 0 || a.kv1 > a.c1 || a.kv0 >= a.kv1) return hipErrorInvalidValue;
-  dim3 grid((unsigned)((a.kv1 - a.kv0 + kKvBKV - 1) / kKvBKV), (unsigned)a.Hkv, (unsigned)a.B);
+  dim3 grid((unsigned)((a.kv1 - a.kv0 + kKvKeys - 1) / kKvKeys), (unsigned)a.Hkv, (unsigned)a.B);
   if (a.D == 128) {
     hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, grid, dim3(256), 0, stream, a);
   } else if (a.D == 64) {
@@ -499,7 +614,7 @@ hipError_t launch_bwd_dkdv_bf16(const ChunkArgs& a, hipStream_t stream) {
 
 hipError_t launch_bwd_dq_bf16(const ChunkArgs& a, hipStream_t stream) {
   const int64_t s = a.c1 - a.c0;
-  dim3 grid((unsigned)((s + kDqBR - 1) / kDqBR), (unsigned)a.Hq, (unsigned)a.B);
+  dim3 grid((unsigned)((s + kDqRows - 1) / kDqRows), (unsigned)a.Hq, (unsigned)a.B);
   if (a.D == 128) {
     hipLaunchKernelGGL(bwd_dq_bf16_kernel<128>, grid, dim3(256), 0, stream, a);
   } else if (a.D == 64) {

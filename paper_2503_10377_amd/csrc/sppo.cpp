@@ -1,7 +1,7 @@
 // libsppo host side: the C ABI declared in include/sppo.h.
 //
-// Owns, per context: the chunk partition (offsets c_0..c_N), a Delta
-// workspace on the device, two non-blocking copy streams (device->host and
+// Owns, per context: the chunk partition (offsets c_0..c_N), a backward
+// workspace on the device (Delta and LSE * log2 e), two non-blocking copy streams (device->host and
 // host->device, default priority), per-chunk events, and page-locked host
 // slots holding each chunk's offload set.  Kernels run on the caller's
 // stream; copies run on the context's streams and are ordered against the
@@ -149,6 +149,7 @@ sppo::ChunkArgs make_args(const sppo_ctx* c, int i) {
   a.D = c->prob.head_dim;
   a.scale = c->scale;
   a.delta = c->delta;
+  a.lse2 = c->delta + (size_t)c->prob.batch * c->prob.n_q_heads * c->s_max;
   a.kv0 = 0;
   a.kv1 = a.c1;
   return a;
@@ -356,8 +357,9 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
   };
   hipError_t e = hipGetDevice(&c->device);
   if (e != hipSuccess) return bail(SPPO_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  // Backward workspace: Delta and LSE * log2(e), [B, Hq, s_max] each.
   const size_t delta_bytes = (size_t)p->batch * p->n_q_heads * c->s_max * sizeof(float);
-  e = hipMalloc(&c->delta, delta_bytes);
+  e = hipMalloc(&c->delta, 2 * delta_bytes);
   if (e != hipSuccess) {
     c->delta = nullptr;
     return bail(e == hipErrorOutOfMemory ? SPPO_ERR_OOM : SPPO_ERR_HIP,

@@ -1,6 +1,6 @@
 // Device-side helpers shared by the gfx950 attention kernels: vector types,
-// the bf16 MFMA wrapper, global->register tile loads, and the swizzled LDS
-// tile layout with its natural and transposed operand reads.
+// the bf16 MFMA wrapper, LDS-DMA tile staging, and the swizzled LDS tile
+// layout with its natural and transposed operand reads.
 //
 // MFMA register layout used throughout (v_mfma_f32_32x32x16_bf16, wave64):
 //   A[i][k] : lane l holds row i = l%32 and 8 k-values in "k-slots"
@@ -19,6 +19,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace sppo {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
@@ -28,6 +30,9 @@ typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 typedef __attribute__((ext_vector_type(4))) short v4i16;
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+template <int I>
+using IC = std::integral_constant<int, I>;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -60,20 +65,24 @@ __device__ __forceinline__ u32x2 pack_bf16x4(float x0, float x1, float x2, float
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
-__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
+// Reductions across the two 32-lane halves of a wave (lane l with l^32):
+// v_permlane32_swap leaves x and its partner in the two results.
+__device__ __forceinline__ float max_xor32(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
-// ------------------------------------------------------ global tile loads
-// A 4-row x 8-column bf16 block held by one thread as four 16-byte words.
-struct Block4x8 {
-  u32x4 r[4];
-};
-
-// Blocks are loaded through a buffer resource based at the first row of a
-// tile: the hardware range check returns zero for every byte offset at or
-// past num_records, so rows >= valid_rows read as zero with no per-lane test,
-// and the per-lane byte offsets stay the same from tile to tile (only the
-// scalar base moves).  Offsets are relative to the tile base, so they fit in
-// 32 bits whatever the tensor size.
+// ------------------------------------------------------ buffer resources
+// Tiles are read through a buffer resource based at the tile's first row:
+// the hardware range check returns zero for every byte offset at or past
+// num_records, so rows >= valid_rows read as zero with no per-lane test, and
+// the per-lane byte offsets stay the same from tile to tile (only the scalar
+// base moves).  Offsets are relative to the tile base, so they fit in 32 bits
+// whatever the tensor size.
 constexpr int kBufferFlags = 0x00020000;  // dword 3 of a raw gfx9 buffer resource
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* tile_base, int64_t valid_rows,
@@ -83,104 +92,111 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* tile
                                            (int)(n * row_stride * (int64_t)sizeof(uint16_t)), kBufferFlags);
 }
 
-// Byte offsets of rows 4*rg + x, columns 8*cg.. of a tile with the given row
-// stride (elements).
-struct Block4x8Offsets {
-  int b[4];
-};
-__device__ __forceinline__ Block4x8Offsets block4x8_offsets(int rg, int cg, int64_t row_stride) {
-  Block4x8Offsets o;
-#pragma unroll
-  for (int x = 0; x < 4; ++x) o.b[x] = (int)(((4 * rg + x) * row_stride + 8 * cg) * (int64_t)sizeof(uint16_t));
-  return o;
+// ------------------------------------------------------------- LDS-DMA
+// buffer_load ... lds moves 16 (or 4) bytes per lane from a buffer resource
+// straight into LDS, lane l's bytes landing at lds + 16 l (4 l): one wave
+// instruction fills 1 KiB of LDS with no VGPR staging and no ds_write.  The
+// loads are issued from inline asm so that the compiler does not treat them
+// as LDS stores it must order (its tracking falls back to waiting for every
+// outstanding load); the kernels order them themselves, each with an
+// explicit s_waitcnt vmcnt(...) followed by a workgroup barrier before any
+// wave reads what another wave loaded.  M0 carries the LDS address; no other
+// code in these kernels uses M0.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
 }
+// (clang warns that M0 is a reserved register; it is only reserved for the
+// compiler's own M0 uses, and these kernels have none.)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t rsrc, void* lds, int voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_addr(lds)), "v"(voff), "s"(rsrc)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void lds_dma4(__amdgpu_buffer_rsrc_t rsrc, void* lds, int voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :
+               : "s"(lds_addr(lds)), "v"(voff), "s"(rsrc)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
 
-__device__ __forceinline__ void load_block4x8(Block4x8& blk, __amdgpu_buffer_rsrc_t rsrc, const Block4x8Offsets& off) {
-#pragma unroll
-  for (int x = 0; x < 4; ++x) blk.r[x] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off.b[x], 0, 0);
-}
+// s_waitcnt immediate that waits for the vector-memory counter to drop to v
+// (expcnt and lgkmcnt left at their maxima).
+__device__ __forceinline__ constexpr int waitcnt_vm(int v) { return (v & 15) | ((v >> 4) << 14) | 0x0F70; }
 
 // ---------------------------------------------------------------- LDS tiles
-// A bf16 tile [rows][D] in LDS is stored in natural layout (row = key or
-// query, column = head dim) with row pitch D + 32 elements, and the 16-byte
-// chunk index c of row r stored at c ^ ((r >> 2) & 3).  The gfx950 LDS has 64
-// four-byte banks; a ds_read_b128 is served 16 lanes at a time, a
-// ds_read_b64 / ds_read_b64_tr_b16 32 lanes at a time, and a ds_write_b128 8
-// lanes at a time.  With this layout every group touches 64 distinct banks
-// (or fewer, disjoint) for the three access patterns used here:
-//   * natural operand reads: 16 consecutive rows, one chunk each -- the
-//     pitch puts rows r and r+1 4 chunks apart (mod 16) and the swizzle
-//     separates r and r+4;
-//   * transposed reads: 4 rows x 4 chunks per 32 lanes, each row's 4 chunks
-//     a distinct quarter of the 256-byte bank window;
-//   * 4x8-block stores: 8 chunks of one row.
-// The swizzle only touches the two low bits of the chunk index, so every
-// access is a per-lane base (one per parity of the k-step for natural reads,
-// one per 8-row half for transposed reads) plus an immediate offset.
+// A bf16 tile [rows][D] is stored unpadded (row pitch D elements), its
+// 16-byte chunk c of row r at physical chunk c ^ f(r).  The gfx950 LDS has 64
+// four-byte banks (256 bytes); a ds_read_b128 is served 16 lanes at a time
+// and a ds_read_b64_tr_b16 32 lanes at a time.  f spreads both access
+// patterns over all 64 banks:
+//   * natural operand reads: 16 consecutive rows, one chunk each -- f is a
+//     bijection on the low 4 bits of the row (D = 128: a row is one bank
+//     window; D = 64: two rows per window, f bijective per row parity);
+//   * transposed reads: 4 consecutive rows x 4 consecutive chunks per 32
+//     lanes -- the rows land in 4 different 64-byte quarters.
+// Rows are written by LDS-DMA in their physical order (1 KiB per wave
+// instruction), so lane l of an instruction fetches the global chunk that
+// belongs at physical position l.
 template <int D>
-struct LdsTile {
-  static constexpr int P = D + 32;
-  static constexpr int CG = D / 8;  // 16-byte chunks per row
-  static __device__ __forceinline__ int swz(int row) { return (row >> 2) & 3; }
-  // Element offset of row 4*rg + x, 16-byte chunk cg.
-  static __device__ __forceinline__ int store_off(int rg, int x, int cg) {
-    return (4 * rg + x) * P + 8 * (cg ^ (rg & 3));
+struct XTile {
+  static constexpr int P = D;         // row pitch, elements
+  static constexpr int CG = D / 8;    // 16-byte chunks per row
+  static constexpr int RPI = 512 / D; // rows per LDS-DMA wave instruction
+  static __device__ __forceinline__ int f(int r) {
+    if constexpr (D == 128) {
+      return ((r & 3) << 2) | ((r >> 2) & 3);
+    } else {
+      return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+    }
   }
-  // Lane bases of natural operand reads: row l%32, chunk 2*kk + l/32, for
-  // even and odd k-steps kk (add rb*P + 32*(kk/2) for row block rb, rb % 32
-  // == 0).
-  struct Nat {
-    int b[2];
-  };
-  static __device__ __forceinline__ Nat nat_base(int lane) {
-    const int l32 = lane & 31, g = lane >> 5, s = swz(l32);
-    return Nat{{l32 * P + 8 * (g ^ s), l32 * P + 8 * ((2 + g) ^ s)}};
+  // Natural operand read of k-step kk for rows rb + l%32 (rb % 32 == 0):
+  // element offset (add rb * P).
+  static __device__ __forceinline__ int nat(int lane, int kk) {
+    const int l32 = lane & 31, g = lane >> 5;
+    return l32 * P + 8 * ((2 * kk + g) ^ f(l32));
   }
-  // Lane bases of a transposed read of rows k0..k0+7 (b[0]) and
-  // k0+8..k0+15 (b[1]); add k0*P (+8*P for b[1]) + x0 with k0 % 16 == 0 and
-  // x0 % 32 == 0.  Source lane s = 16q + 4e + a supplies the 8 bytes at row
-  // 4*(q/2) + e, column 16*(q%2) + 4*a; ds_read_b64_tr_b16 hands output lane
+  // Transposed read of rows k0 + {0..7} (hi = 0) or k0 + {8..15} (hi = 1),
+  // columns 32 db..32 db+31 (add k0 * P, k0 % 16 == 0).  Source lane
+  // s = 16q + 4e + a supplies the 8 bytes at row 4(q/2) + e, columns
+  // 16(q%2) + 4a of the 16x32 block; ds_read_b64_tr_b16 hands output lane
   // 16q + 4a' + b element b of source lanes 16q + 4e + a', e = 0..3.
-  struct Tr {
-    int b[2];
-  };
-  static __device__ __forceinline__ Tr tr_base(int lane) {
+  static __device__ __forceinline__ int tr(int lane, int db, int hi) {
     const int q = lane >> 4, e = (lane >> 2) & 3, a = lane & 3;
-    const int row = 4 * (q >> 1) + e, c = 2 * (q & 1) + (a >> 1);
-    return Tr{{row * P + 8 * (c ^ (q >> 1)) + 4 * (a & 1), row * P + 8 * (c ^ ((q >> 1) + 2)) + 4 * (a & 1)}};
+    const int row = 4 * (q >> 1) + e + 8 * hi;
+    const int c = 4 * db + 2 * (q & 1) + (a >> 1);
+    return row * P + 8 * (c ^ f(row)) + 4 * (a & 1);
+  }
+  // Byte offset, relative to the first row of a tile in global memory, of
+  // the chunk lane `lane` fetches in LDS-DMA instruction u of the tile.
+  static __device__ __forceinline__ int dma(int lane, int u, int64_t row_stride) {
+    const int row = RPI * u + lane / CG, p = lane % CG;
+    return (int)((row * row_stride + 8 * (p ^ f(row))) * (int64_t)sizeof(uint16_t));
   }
 };
-
-template <int D>
-__device__ __forceinline__ void store_block_tile(const Block4x8& blk, uint16_t* tile, int rg, int cg) {
-#pragma unroll
-  for (int x = 0; x < 4; ++x) {
-    *reinterpret_cast<u32x4*>(tile + LdsTile<D>::store_off(rg, x, cg)) = blk.r[x];
-  }
-}
-
-// Natural operand: lane l gets row rb + l%32, columns 16*kk + 8*(l/32) + 0..7.
-template <int D>
-__device__ __forceinline__ bf16x8 ld_lds_nat(const uint16_t* tile, const typename LdsTile<D>::Nat& nat, int rb,
-                                             int kk) {
-  return as_bf16x8(*reinterpret_cast<const u32x4*>(tile + nat.b[kk & 1] + rb * LdsTile<D>::P + 32 * (kk >> 1)));
-}
 
 __device__ __forceinline__ v4i16 ds_read_tr16(const uint16_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
 }
 
-// Transposed operand from a natural tile: lane l gets column x0 + l%32 and
-// rows k0 + {8*(e/4) + 4*(l/32) + e%4 : e = 0..7}, i.e. the permuted k-slot
-// map, so it pairs with an operand taken from C-tile registers.
-template <int D>
-__device__ __forceinline__ bf16x8 ld_lds_tr(const uint16_t* tile, const typename LdsTile<D>::Tr& tr, int k0, int x0) {
-  constexpr int P = LdsTile<D>::P;
-  const v4i16 lo = ds_read_tr16(tile + tr.b[0] + k0 * P + x0);
-  const v4i16 hi = ds_read_tr16(tile + tr.b[1] + (k0 + 8) * P + x0);
-  const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
-  const u32x4 r = {l2.x, l2.y, h2.x, h2.y};
-  return as_bf16x8(r);
+// Natural operand: lane l gets row l%32, columns 16 kk + 8 (l/32) + 0..7 of
+// the 32-row block at X (offset from XTile::nat).
+__device__ __forceinline__ bf16x8 ld_nat(const uint16_t* X, int off) {
+  return as_bf16x8(*reinterpret_cast<const u32x4*>(X + off));
+}
+
+// Transposed operand from a natural tile: lane l gets column l%32 of the
+// 32-column block and rows {8(e/4) + 4(l/32) + e%4 : e = 0..7} of the 16-row
+// block, i.e. the permuted k-slot map, so it pairs with an operand taken
+// from C-tile registers.  lo/hi: XTile::tr offsets plus the block's row base.
+__device__ __forceinline__ bf16x8 ld_tr(const uint16_t* X, int lo, int hi) {
+  const v4i16 a = ds_read_tr16(X + lo);
+  const v4i16 b = ds_read_tr16(X + hi);
+  const u32x2 a2 = __builtin_bit_cast(u32x2, a), b2 = __builtin_bit_cast(u32x2, b);
+  return as_bf16x8(u32x4{a2.x, a2.y, b2.x, b2.y});
 }
 
 }  // namespace sppo

@@ -159,9 +159,37 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
                                                       __builtin_amdgcn_readfirstlane((int)(nrec * 4)), kBufferFlags);
     if (lane < 16) lds_dma4(rl, ld + ldst, dmal);
   };
-  // Stream position n of head h -> sub-block sb_u + n; past the stream: zeros.
-  auto stream_issue = [&](int h, int n, uint16_t* qd, uint16_t* od, float* ld) {
-    issue(h, n < N ? sb_u + n : nsb, qd, od, ld);
+  // The unmasked stream of a head issues its sub-blocks in order, so the
+  // scalar state below walks Q, dO and the record one sub-block per call
+  // (no per-call index arithmetic).  Past the chunk end the byte counts drop
+  // to zero and the DMA fills zeros.
+  const int64_t sbb = (int64_t)kSB * qstride * 2;  // bytes per sub-block of Q or dO
+  const int qrow_bytes = (int)(qstride * 2);
+  uint64_t qa = 0, oa = 0, la = 0;
+  int rem = 0;
+  auto stream_begin = [&](int h) {
+    const int64_t r0 = (int64_t)sb_u * kSB;
+    const int64_t tile0 = (b * s + r0) * a.Hq + h;
+    qa = reinterpret_cast<uint64_t>(static_cast<const uint16_t*>(a.q) + tile0 * D);
+    oa = reinterpret_cast<uint64_t>(static_cast<const uint16_t*>(a.dout) + tile0 * D);
+    la = reinterpret_cast<uint64_t>(lsrc + (b * a.Hq + h) * s + r0);
+    rem = (int)(s - r0);
+  };
+  auto stream_issue = [&](uint16_t* qd, uint16_t* od, float* ld) {
+    const int n = rem <= 0 ? 0 : (rem < kSB ? rem : kSB);
+    const auto rq = uniform_rsrc(qa, n * qrow_bytes);
+    const auto ro = uniform_rsrc(oa, n * qrow_bytes);
+#pragma unroll
+    for (int x = 0; x < IPWQ; ++x) {
+      lds_dma16(rq, qd + (w * IPWQ + x) * 512, dmaq[x]);
+      lds_dma16(ro, od + (w * IPWQ + x) * 512, dmaq[x]);
+    }
+    const auto rl = uniform_rsrc(la, n * 4);
+    if (lane < 16) lds_dma4(rl, ld + ldst, dmal);
+    qa += sbb;
+    oa += sbb;
+    la += kSB * 4;
+    rem -= kSB;
   };
   auto tr_rd = [&](const uint16_t* X, int hh, int db) {
     return ld_tr(X, tro[db][0] + 16 * hh * P, tro[db][1] + 16 * hh * P);
@@ -224,11 +252,12 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
     // ---- unmasked stream, software pipelined
     if (N == 0) continue;
     __syncthreads();  // every slot is free
-    stream_issue(h, 0, qbuf(IC<0>{}), obuf(IC<0>{}), lbuf(IC<0>{}));
-    stream_issue(h, 1, qbuf(IC<1>{}), obuf(IC<1>{}), lbuf(IC<1>{}));
-    stream_issue(h, 2, qbuf(IC<2>{}), obuf(IC<2>{}), lbuf(IC<2>{}));
-    stream_issue(h, 3, qbuf(IC<3>{}), obuf(IC<3>{}), lbuf(IC<3>{}));
-    stream_issue(h, 4, qbuf(IC<4>{}), obuf(IC<4>{}), lbuf(IC<4>{}));
+    stream_begin(h);
+    stream_issue(qbuf(IC<0>{}), obuf(IC<0>{}), lbuf(IC<0>{}));
+    stream_issue(qbuf(IC<1>{}), obuf(IC<1>{}), lbuf(IC<1>{}));
+    stream_issue(qbuf(IC<2>{}), obuf(IC<2>{}), lbuf(IC<2>{}));
+    stream_issue(qbuf(IC<3>{}), obuf(IC<3>{}), lbuf(IC<3>{}));
+    stream_issue(qbuf(IC<4>{}), obuf(IC<4>{}), lbuf(IC<4>{}));
     __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - 1) * DMA_PER_SB));
     __syncthreads();
     f32x16 sa, da, sb2, db2;
@@ -242,7 +271,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
       constexpr int I1 = (I + 1) % kRing, I5 = (I + kAhead) % kRing;
       __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - 2) * DMA_PER_SB));
       __syncthreads();
-      stream_issue(h, n + kAhead, qbuf(IC<I5>{}), obuf(IC<I5>{}), lbuf(IC<I5>{}));
+      stream_issue(qbuf(IC<I5>{}), obuf(IC<I5>{}), lbuf(IC<I5>{}));
       const uint16_t* Qn = qbuf(IC<I1>{});
       const uint16_t* On = obuf(IC<I1>{});
       const uint16_t* Qc = qbuf(IC<I>{});
@@ -429,15 +458,24 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
 
   // DMA of K/V sub-block u (keys [32u, 32u+32)) into a slot; keys past the
   // chunk end load zeros, so every call issues DMA_PER_SB instructions.
-  auto issue = [&](int u, uint16_t* dst) {
-    const int64_t k0 = (int64_t)u * kSB;
-    const auto rk = tile_rsrc(kbase + k0 * kvstride, c1 - k0, kSB, kvstride);
-    const auto rv = tile_rsrc(vbase + k0 * kvstride, c1 - k0, kSB, kvstride);
+  // Sub-blocks are issued in key order, so scalar state walks K and V one
+  // sub-block per call.
+  const int64_t sbb = (int64_t)kSB * kvstride * 2;  // bytes per sub-block of K or V
+  const int krow_bytes = (int)(kvstride * 2);
+  uint64_t ka = reinterpret_cast<uint64_t>(kbase), va = reinterpret_cast<uint64_t>(vbase);
+  int remk = (int)c1;  // keys [k0, c1) are valid
+  auto issue_next = [&](uint16_t* dst) {
+    const int n = remk <= 0 ? 0 : (remk < kSB ? remk : kSB);
+    const auto rk = uniform_rsrc(ka, n * krow_bytes);
+    const auto rv = uniform_rsrc(va, n * krow_bytes);
 #pragma unroll
     for (int x = 0; x < IPWK; ++x) {
       lds_dma16(rk, dst + (w * IPWK + x) * 512, dmak[x]);
       lds_dma16(rv, dst + kSB * P + (w * IPWK + x) * 512, dmak[x]);
     }
+    ka += sbb;
+    va += sbb;
+    remk -= kSB;
   };
   auto tr_rd = [&](const uint16_t* X, int hh, int db) {
     return ld_tr(X, tro[db][0] + 16 * hh * P, tro[db][1] + 16 * hh * P);
@@ -456,11 +494,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
 
   // Prologue: sub-blocks 0..4 (which also covers every diagonal sub-block
   // when N is 0).
-  issue(0, R0);
-  issue(1, R1);
-  issue(2, R2);
-  issue(3, R3);
-  issue(4, R4);
+  issue_next(R0);
+  issue_next(R1);
+  issue_next(R2);
+  issue_next(R3);
+  issue_next(R4);
 
   if (N > 0) {
     __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - 1) * DMA_PER_SB));
@@ -475,7 +513,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
       constexpr int I1 = (I + 1) % kRing, I5 = (I + kAhead) % kRing;
       __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - 2) * DMA_PER_SB));
       __syncthreads();
-      issue(n + kAhead, slot(IC<I5>{}));
+      issue_next(slot(IC<I5>{}));  // sub-block n + kAhead
       const uint16_t* Kn = slot(IC<I1>{});
       const uint16_t* Vn = Kn + kSB * P;
       const uint16_t* Kc = slot(IC<I>{});

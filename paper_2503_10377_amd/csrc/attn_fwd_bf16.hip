@@ -99,19 +99,27 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
   const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + (b * a.S * a.Hkv + hk) * D;
   const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + (b * a.S * a.Hkv + hk) * D;
 
-  // K sub-block u (keys [32u, 32u+32)) and V tile j (keys [64j, 64j+64)) into
-  // LDS; keys past the chunk end load as zeros.
-  auto issue_k = [&](int u, uint16_t* dst) {
-    const int64_t k0 = (int64_t)u * 32;
-    const auto rk = tile_rsrc(kbase + k0 * kvstride, c1 - k0, 32, kvstride);
+  // The next K sub-block (32 keys) or V tile (64 keys) into LDS; keys past
+  // the chunk end load as zeros.  Both are issued in key order, so scalar
+  // state walks K and V (no per-call index arithmetic).
+  const int krow_bytes = (int)(kvstride * 2);
+  uint64_t ka = reinterpret_cast<uint64_t>(kbase), va = reinterpret_cast<uint64_t>(vbase);
+  int remk = (int)c1, remv = (int)c1;  // keys left from the next sub-block / tile
+  auto issue_k = [&](uint16_t* dst) {
+    const int n = remk <= 0 ? 0 : (remk < 32 ? remk : 32);
+    const auto rk = uniform_rsrc(ka, n * krow_bytes);
 #pragma unroll
     for (int x = 0; x < IPWK; ++x) lds_dma16(rk, dst + (w * IPWK + x) * 512, dmak[x]);
+    ka += (uint64_t)32 * krow_bytes;
+    remk -= 32;
   };
-  auto issue_v = [&](int j, uint16_t* dst) {
-    const int64_t k0 = (int64_t)j * BC;
-    const auto rv = tile_rsrc(vbase + k0 * kvstride, c1 - k0, BC, kvstride);
+  auto issue_v = [&](uint16_t* dst) {
+    const int n = remv <= 0 ? 0 : (remv < BC ? remv : BC);
+    const auto rv = uniform_rsrc(va, n * krow_bytes);
 #pragma unroll
     for (int x = 0; x < IPWV; ++x) lds_dma16(rv, dst + (w * IPWV + x) * 512, dmav[x]);
+    va += (uint64_t)BC * krow_bytes;
+    remv -= BC;
   };
 
   f32x16 o[ND];
@@ -205,10 +213,10 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
   };
 
   // Prologue: K sub-blocks 0..2 and V tile 0.
-  issue_k(0, K0);
-  issue_v(0, V0);
-  if (1 < nsub) issue_k(1, K1);
-  if (2 < nsub) issue_k(2, K2);
+  issue_k(K0);
+  issue_v(V0);
+  if (1 < nsub) issue_k(K1);
+  if (2 < nsub) issue_k(K2);
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   __syncthreads();
   int klast = nsub < 3 ? nsub - 1 : 2, vlast = 0;  // last K sub-block / V tile issued
@@ -221,9 +229,9 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
     for (int kk = 1; kk < NK; ++kk) sa = mfma32(ld_nat(K0, nat[kk]), qf[kk], sa);
     rescale_if_needed(row_max(sa));
     __syncthreads();  // every wave is done with K0 before sub-block 4 lands there
-    if (3 < nsub) issue_k(3, K3);
-    if (4 < nsub) issue_k(4, K0);
-    if (1 < nkv) issue_v(1, V1);
+    if (3 < nsub) issue_k(K3);
+    if (4 < nsub) issue_k(K0);
+    if (1 < nkv) issue_v(V1);
     // Tile j, parity PAR (every LDS base an immediate): sub-blocks 2j (S^T in
     // sa) and 2j+1 (S^T in sb).  At its start K sub-blocks <= 2j+2 and V tile
     // j have landed; sub-blocks 2j-1, 2j and V tile j-1 are free for
@@ -233,9 +241,9 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
       if (j > 0) {
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
         __syncthreads();
-        if (2 * j + 3 < nsub) issue_k(2 * j + 3, kbuf(IC<(2 * PAR + 3) & 3>{}));
-        if (2 * j + 4 < nsub) issue_k(2 * j + 4, kbuf(IC<(2 * PAR) & 3>{}));
-        if (j + 1 < nkv) issue_v(j + 1, vbuf(IC<(PAR + 1) & 1>{}));
+        if (2 * j + 3 < nsub) issue_k(kbuf(IC<(2 * PAR + 3) & 3>{}));
+        if (2 * j + 4 < nsub) issue_k(kbuf(IC<(2 * PAR) & 3>{}));
+        if (j + 1 < nkv) issue_v(vbuf(IC<(PAR + 1) & 1>{}));
       }
       const uint16_t* V = vbuf(IC<PAR>{});
       rescale_if_needed(step(sa, sb, kbuf(IC<(2 * PAR + 1) & 3>{}), V));
@@ -257,10 +265,10 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
   for (int j = nfull; j < nkv; ++j) {
     if (j > nfull) {
       __syncthreads();  // every wave is done with tile j-1
-      for (int u = klast + 1; u <= 2 * j + 1 && u < nsub; ++u) issue_k(u, kbuf_rt(u & 3));
+      for (int u = klast + 1; u <= 2 * j + 1 && u < nsub; ++u) issue_k(kbuf_rt(u & 3));
       if (2 * j + 1 > klast) klast = 2 * j + 1 < nsub - 1 ? 2 * j + 1 : nsub - 1;
       if (j > vlast) {
-        issue_v(j, (j & 1) ? V1 : V0);
+        issue_v((j & 1) ? V1 : V0);
         vlast = j;
       }
     }

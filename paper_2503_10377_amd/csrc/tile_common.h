@@ -87,9 +87,18 @@ constexpr int kBufferFlags = 0x00020000;  // dword 3 of a raw gfx9 buffer resour
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* tile_base, int64_t valid_rows,
                                                             int tile_rows, int64_t row_stride) {
-  const int64_t n = valid_rows <= 0 ? 0 : (valid_rows < tile_rows ? valid_rows : tile_rows);
+  const int n = valid_rows <= 0 ? 0 : (valid_rows < tile_rows ? (int)valid_rows : tile_rows);
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(tile_base), (short)0,
-                                           (int)(n * row_stride * (int64_t)sizeof(uint16_t)), kBufferFlags);
+                                           n * (int)(row_stride * (int64_t)sizeof(uint16_t)), kBufferFlags);
+}
+
+// Buffer resource over the nbytes bytes at byte address addr, with every
+// field made wave-uniform (a buffer instruction takes it in scalar registers).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(uint64_t addr, int nbytes) {
+  const uint64_t u = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(addr >> 32)) << 32) |
+                     (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)addr);
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(u), (short)0,
+                                           __builtin_amdgcn_readfirstlane(nbytes), kBufferFlags);
 }
 
 // ------------------------------------------------------------- LDS-DMA
@@ -103,7 +112,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* tile
 // wave reads what another wave loaded.  M0 carries the LDS address; no other
 // code in these kernels uses M0.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
+  // A generic pointer into LDS is the shared aperture (high half) plus the
+  // LDS offset (low half); truncating skips the null check of a cast.
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
 }
 // (clang warns that M0 is a reserved register; it is only reserved for the
 // compiler's own M0 uses, and these kernels have none.)

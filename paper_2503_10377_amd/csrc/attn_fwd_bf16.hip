@@ -147,10 +147,9 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
   // Row max (scaled to base 2) of a 32-key S^T block: 16 keys in-lane, the
   // other 16 in lane^32.
   auto row_max = [&](const f32x16& x) {
-    float m4[4];
-#pragma unroll
-    for (int y = 0; y < 4; ++y) m4[y] = fmaxf(fmaxf(x[4 * y], x[4 * y + 1]), fmaxf(x[4 * y + 2], x[4 * y + 3]));
-    return max_xor32(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]))) * C;
+    const float a = max3_nc(x[0], x[1], x[2]), b = max3_nc(x[3], x[4], x[5]), c = max3_nc(x[6], x[7], x[8]);
+    const float d = max3_nc(x[9], x[10], x[11]), e = max3_nc(x[12], x[13], x[14]);
+    return max_xor32(max_nc(max3_nc(a, b, c), max3_nc(d, e, x[15]))) * C;
   };
   auto ld_vt = [&](const uint16_t* V, int db, int kb) {
     return ld_tr(V, tro[db][0] + 16 * kb * P, tro[db][1] + 16 * kb * P);

@@ -65,11 +65,20 @@ __device__ __forceinline__ u32x2 pack_bf16x4(float x0, float x1, float x2, float
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
+// IEEE maximum (NaN-propagating): fmaxf's maxNum must quiet signalling NaNs
+// first, so in IEEE mode it puts a v_max_f32 x, x, x in front of every
+// operand it cannot prove canonical (all MFMA results); maximum needs no such
+// step, and gfx950 evaluates three operands per v_maximum3_f32.
+__device__ __forceinline__ float max3_nc(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+__device__ __forceinline__ float max_nc(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
 // Reductions across the two 32-lane halves of a wave (lane l with l^32):
 // v_permlane32_swap leaves x and its partner in the two results.
 __device__ __forceinline__ float max_xor32(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return max_nc(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float sum_xor32(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);

@@ -170,9 +170,9 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   auto stream_begin = [&](int h) {
     const int64_t r0 = (int64_t)sb_u * kSB;
     const int64_t tile0 = (b * s + r0) * a.Hq + h;
-    qa = reinterpret_cast<uint64_t>(static_cast<const uint16_t*>(a.q) + tile0 * D);
-    oa = reinterpret_cast<uint64_t>(static_cast<const uint16_t*>(a.dout) + tile0 * D);
-    la = reinterpret_cast<uint64_t>(lsrc + (b * a.Hq + h) * s + r0);
+    qa = uniform_u64(reinterpret_cast<uint64_t>(static_cast<const uint16_t*>(a.q) + tile0 * D));
+    oa = uniform_u64(reinterpret_cast<uint64_t>(static_cast<const uint16_t*>(a.dout) + tile0 * D));
+    la = uniform_u64(reinterpret_cast<uint64_t>(lsrc + (b * a.Hq + h) * s + r0));
     rem = (int)(s - r0);
   };
   auto stream_issue = [&](uint16_t* qd, uint16_t* od, float* ld) {
@@ -462,7 +462,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
   // sub-block per call.
   const int64_t sbb = (int64_t)kSB * kvstride * 2;  // bytes per sub-block of K or V
   const int krow_bytes = (int)(kvstride * 2);
-  uint64_t ka = reinterpret_cast<uint64_t>(kbase), va = reinterpret_cast<uint64_t>(vbase);
+  uint64_t ka = uniform_u64(reinterpret_cast<uint64_t>(kbase)), va = uniform_u64(reinterpret_cast<uint64_t>(vbase));
   int remk = (int)c1;  // keys [k0, c1) are valid
   auto issue_next = [&](uint16_t* dst) {
     const int n = remk <= 0 ? 0 : (remk < kSB ? remk : kSB);

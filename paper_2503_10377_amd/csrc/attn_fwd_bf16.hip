@@ -103,7 +103,7 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
   // the chunk end load as zeros.  Both are issued in key order, so scalar
   // state walks K and V (no per-call index arithmetic).
   const int krow_bytes = (int)(kvstride * 2);
-  uint64_t ka = reinterpret_cast<uint64_t>(kbase), va = reinterpret_cast<uint64_t>(vbase);
+  uint64_t ka = uniform_u64(reinterpret_cast<uint64_t>(kbase)), va = uniform_u64(reinterpret_cast<uint64_t>(vbase));
   int remk = (int)c1, remv = (int)c1;  // keys left from the next sub-block / tile
   auto issue_k = [&](uint16_t* dst) {
     const int n = remk <= 0 ? 0 : (remk < 32 ? remk : 32);

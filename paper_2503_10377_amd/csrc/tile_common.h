@@ -101,12 +101,18 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* tile
                                            n * (int)(row_stride * (int64_t)sizeof(uint16_t)), kBufferFlags);
 }
 
+// A wave-uniform 64-bit value moved to scalar registers (64-bit products
+// are formed by the VALU, so an address computed from uniform values can
+// still sit in VGPRs; a scalar copy keeps later updates on the SALU).
+__device__ __forceinline__ uint64_t uniform_u64(uint64_t x) {
+  return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(x >> 32)) << 32) |
+         (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)x);
+}
+
 // Buffer resource over the nbytes bytes at byte address addr, with every
 // field made wave-uniform (a buffer instruction takes it in scalar registers).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(uint64_t addr, int nbytes) {
-  const uint64_t u = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(addr >> 32)) << 32) |
-                     (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)addr);
-  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(u), (short)0,
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(uniform_u64(addr)), (short)0,
                                            __builtin_amdgcn_readfirstlane(nbytes), kBufferFlags);
 }
 

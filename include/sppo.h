@@ -99,6 +99,14 @@ typedef struct {
   sppo_dtype dtype;              /* element type of Q, K, V, O, dO, dQ      */
   float softmax_scale;           /* 0 means 1/sqrt(D)                       */
   sppo_offload offload;          /* offload set; NONE allocates no host mem */
+  int32_t n_extra;               /* 0..16 further saved-activation planes
+                                    that travel with Q/O/LSE (the rest of a
+                                    full layer's saved tensors, Sec. 5.1:
+                                    everything but K/V is offloadable)      */
+  const size_t* extra_row_bytes; /* host array of n_extra row sizes (bytes
+                                    per token, > 0); plane k of chunk i is a
+                                    chunk-local [B, s_i, extra_row_bytes[k]]
+                                    byte array; NULL when n_extra == 0      */
 } sppo_problem;
 
 /* Device pointers of one chunk's saved activations, for offload/prefetch. */
@@ -108,6 +116,8 @@ typedef struct {
   float* lse;   /* LSE_i [B, Hq, s_i]     chunk-local                        */
   void* k;      /* base of the full K cache [B, S, Hkv, D]; rows of chunk i  */
   void* v;      /* base of the full V cache [B, S, Hkv, D]; rows of chunk i  */
+  void* const* extra; /* n_extra device pointers (planes of chunk i), or
+                         NULL when the problem has no extra planes          */
 } sppo_chunk_bufs;
 
 typedef struct {
@@ -286,6 +296,81 @@ const char* sppo_last_error(const sppo_ctx* ctx);
 
 /* Static name of a status code. */
 const char* sppo_status_string(sppo_status s);
+
+/* ------------------------------------------------------------------------
+ * Full-layer building blocks.  A transformer layer chunk (Sec. 5.1: the
+ * subsequence's tensors of one layer -- LayerNorm, the QKV projection,
+ * attention, the output projection and the MLP; Sec. 3.3: attention and the
+ * GEMMs are the compute-bound operators) is composed from the attention
+ * calls above and the calls below.  They need no context: each validates
+ * its arguments on the host, enqueues on `stream` and returns a status
+ * (INVALID_ARG, UNSUPPORTED or HIP); nothing is enqueued on failure.
+ * Activations are bf16, statistics and parameter gradients fp32, every
+ * pointer a device pointer, 16-byte aligned where it is bf16 data, every
+ * leading dimension (ld*, in elements) a multiple of 8.
+ * ---------------------------------------------------------------------- */
+
+/* C[M, N] (op)= sum_k A(m, k) B(k, n), bf16 operands, fp32 accumulation.
+ *   SPPO_GEMM_NT: A is [M, K] (row stride lda), B is [N, K] (ldb), so
+ *                 C = A B^T; K % 64 == 0.  x W = x (W^T)^T with W^T
+ *                 [out, in], and dY W^T with W [in, out].
+ *   SPPO_GEMM_TN: A is stored [K, M], B stored [K, N], so C = A^T B;
+ *                 M % 256 == 0, N % 256 == 0.  The weight gradient X^T dY.
+ * Rows past M (NT) or K (TN) read as zero, only C[m < M][n < N] is
+ * written.  Epilogues (aux: bf16 [M, N] with row stride ldaux):
+ *   BF16      C = acc (bf16)
+ *   ADD_BF16  C = acc + aux (bf16): the residual add
+ *   GELU      aux = bf16(acc) (the pre-activation, kept for the backward),
+ *             C = gelu(aux) with gelu(a) = a/2 (1 + tanh(sqrt(2/pi)(a +
+ *             0.044715 a^3)))
+ *   DGELU     C = acc * gelu'(aux) (bf16)
+ *   ACC_F32   C += acc (fp32): gradients accumulated over chunks
+ *   F32       C = acc (fp32) */
+typedef enum { SPPO_GEMM_NT = 0, SPPO_GEMM_TN = 1 } sppo_gemm_layout;
+typedef enum {
+  SPPO_EPI_BF16 = 0,
+  SPPO_EPI_ADD_BF16 = 1,
+  SPPO_EPI_GELU = 2,
+  SPPO_EPI_DGELU = 3,
+  SPPO_EPI_ACC_F32 = 4,
+  SPPO_EPI_F32 = 5
+} sppo_epilogue;
+sppo_status sppo_gemm_bf16(int32_t layout, int64_t M, int64_t N, int64_t K, const void* a, int64_t lda,
+                           const void* b, int64_t ldb, void* c, int64_t ldc, int32_t epilogue, void* aux,
+                           int64_t ldaux, void* stream);
+
+/* LayerNorm of `rows` rows of H (H % 8 == 0, H <= 8192):
+ * y = (x - mean) * rstd * gamma + beta, rstd = 1/sqrt(var + eps) with the
+ * biased variance; mean and rstd (fp32 [rows]) are written for the
+ * backward.  gamma, beta fp32 [H]. */
+sppo_status sppo_layernorm_fwd(int64_t rows, int32_t H, const void* x, int64_t ldx, const float* gamma,
+                               const float* beta, float eps, void* y, int64_t ldy, float* mean, float* rstd,
+                               void* stream);
+
+/* Backward of the LayerNorm above, with the residual branch folded in:
+ *   dx = dres + rstd * (g - mean_j g - xhat * mean_j(g xhat)),
+ *   g = dy * gamma, xhat = (x - mean) * rstd,
+ * and dgamma += sum_rows dy * xhat, dbeta += sum_rows dy (fp32 [H],
+ * accumulated in a fixed order, so results are reproducible bit for bit).
+ * workspace: device fp32 scratch of sppo_layernorm_bwd_workspace bytes. */
+size_t sppo_layernorm_bwd_workspace(int64_t rows, int32_t H);
+sppo_status sppo_layernorm_bwd(int64_t rows, int32_t H, const void* x, int64_t ldx, const float* gamma,
+                               const float* mean, const float* rstd, const void* dy, int64_t lddy,
+                               const void* dres, int64_t lddres, void* dx, int64_t lddx, float* dgamma,
+                               float* dbeta, float* workspace, size_t workspace_bytes, void* stream);
+
+/* y = gelu(x) (the tanh form above) over n bf16 values, n % 8 == 0. */
+sppo_status sppo_gelu_bf16(const void* x, void* y, int64_t n, void* stream);
+
+/* out [cols, rows] = in [rows, cols]^T, bf16, both contiguous. */
+sppo_status sppo_transpose_bf16(const void* in, void* out, int64_t rows, int64_t cols, void* stream);
+
+/* Row t < rows of out [rows, wq + 2 wkv] (bf16) = [dq[t] | dk[row0 + t] |
+ * dv[row0 + t]]: the chunk's dQ (bf16 [rows, wq]) beside its rows of the
+ * fp32 dK/dV accumulators ([.., wkv]) rounded to bf16 -- the gradient of
+ * the fused QKV projection's output (B = 1). */
+sppo_status sppo_pack_qkv_grad(int64_t rows, int32_t wq, int32_t wkv, const void* dq, const float* dk,
+                               const float* dv, int64_t row0, void* out, void* stream);
 
 #ifdef __cplusplus
 }

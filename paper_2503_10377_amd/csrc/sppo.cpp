@@ -48,6 +48,7 @@ struct HostSlot {
   void* lse = nullptr;
   void* k = nullptr;
   void* v = nullptr;
+  std::vector<void*> extra;  // extra planes, same order as the problem's
 };
 
 }  // namespace
@@ -55,6 +56,7 @@ struct HostSlot {
 struct sppo_ctx {
   sppo_problem prob{};
   std::vector<int64_t> off;
+  std::vector<size_t> extra_rb;  // row bytes of the extra planes
   int64_t s_max = 0;
   size_t elt = 0;
   float scale = 0.f;
@@ -138,6 +140,16 @@ sppo_status check_ptr(sppo_ctx* ctx, const void* p, const char* name) {
   return SPPO_OK;
 }
 
+sppo_status check_extra(sppo_ctx* ctx, void* const* extra, const char* name) {
+  if (ctx->extra_rb.empty()) return SPPO_OK;
+  if (!extra) return fail(ctx, SPPO_ERR_INVALID_ARG, std::string(name) + " is null but the problem has extra planes");
+  for (size_t k = 0; k < ctx->extra_rb.size(); ++k) {
+    sppo_status st = check_ptr(ctx, extra[k], name);
+    if (st != SPPO_OK) return st;
+  }
+  return SPPO_OK;
+}
+
 sppo::ChunkArgs make_args(const sppo_ctx* c, int i) {
   sppo::ChunkArgs a{};
   a.B = c->prob.batch;
@@ -189,8 +201,8 @@ hipError_t copy_rows(void* dst, size_t dpitch, const void* src, size_t spitch, s
 //   Q_i, O_i [B, s_i, Hq, D]: B spans of r*Hq*D elements, pitch s_i*Hq*D
 //   LSE_i   [B, Hq, s_i]    : B*Hq spans of r floats, pitch s_i
 // Returns the bytes moved through *bytes.
-hipError_t move_qol(sppo_ctx* c, int i, int64_t r, void* q, void* o, float* lse, bool to_host, hipStream_t s,
-                    uint64_t* bytes) {
+hipError_t move_qol(sppo_ctx* c, int i, int64_t r, void* q, void* o, float* lse, void* const* extra, bool to_host,
+                    hipStream_t s, uint64_t* bytes) {
   const size_t row = (size_t)c->prob.n_q_heads * c->prob.head_dim * c->elt;
   const size_t si = (size_t)chunk_len(c, i), B = (size_t)c->prob.batch, BH = B * c->prob.n_q_heads;
   const hipMemcpyKind kind = to_host ? hipMemcpyDeviceToHost : hipMemcpyHostToDevice;
@@ -207,6 +219,13 @@ hipError_t move_qol(sppo_ctx* c, int i, int64_t r, void* q, void* o, float* lse,
     e = to_host ? copy_rows(h.lse, lp, lse, lp, lw, BH, kind, s) : copy_rows(lse, lp, h.lse, lp, lw, BH, kind, s);
   }
   *bytes = 2 * (uint64_t)r * row * B + (uint64_t)r * sizeof(float) * BH;
+  // extra planes [B, s_i, rb]: B spans of r*rb bytes, pitch s_i*rb
+  for (size_t k = 0; k < c->extra_rb.size() && e == hipSuccess; ++k) {
+    const size_t rb = c->extra_rb[k];
+    e = to_host ? copy_rows(h.extra[k], si * rb, extra[k], si * rb, r * rb, B, kind, s)
+                : copy_rows(extra[k], si * rb, h.extra[k], si * rb, r * rb, B, kind, s);
+    *bytes += (uint64_t)r * rb * B;
+  }
   return e;
 }
 
@@ -323,6 +342,12 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
       p->offload != SPPO_OFFLOAD_QKVOL_EVICT) {
     return fail(nullptr, SPPO_ERR_INVALID_ARG, "unknown offload mode");
   }
+  if (p->n_extra < 0 || p->n_extra > 16 || (p->n_extra > 0 && !p->extra_row_bytes)) {
+    return fail(nullptr, SPPO_ERR_INVALID_ARG, "n_extra must be 0..16 with extra_row_bytes given");
+  }
+  for (int k = 0; k < p->n_extra; ++k) {
+    if (p->extra_row_bytes[k] == 0) return fail(nullptr, SPPO_ERR_INVALID_ARG, "extra_row_bytes must be > 0");
+  }
   if (!(p->softmax_scale >= 0.f) || std::isinf(p->softmax_scale)) {
     return fail(nullptr, SPPO_ERR_INVALID_ARG, "softmax_scale must be finite and >= 0 (0 = 1/sqrt(D))");
   }
@@ -346,6 +371,8 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
   if (!c) return fail(nullptr, SPPO_ERR_OOM, "host allocation of the context failed");
   c->prob = *p;
   c->prob.chunk_offsets = nullptr;
+  c->prob.extra_row_bytes = nullptr;
+  c->extra_rb.assign(p->extra_row_bytes, p->extra_row_bytes + p->n_extra);
   c->off = std::move(off);
   c->elt = p->dtype == SPPO_BF16 ? 2 : 4;
   c->scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / std::sqrt((float)p->head_dim);
@@ -398,7 +425,9 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
       const size_t bq = bytes_q(c, i), bl = bytes_lse(c, i);
       const size_t bkv = offload_kv(c) ? bytes_kv_row_block(c, i) * p->batch : 0;
       auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-      const size_t total = 2 * up(bq) + up(bl) + 2 * up(bkv);
+      size_t bx = 0;
+      for (size_t rb : c->extra_rb) bx += up(rb * (size_t)chunk_len(c, i) * (size_t)p->batch);
+      const size_t total = 2 * up(bq) + up(bl) + 2 * up(bkv) + bx;
       void* base = nullptr;
       e = hipHostMalloc(&base, total, hipHostMallocDefault);
       if (e != hipSuccess || !base) {
@@ -414,6 +443,11 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
       if (bkv) {
         s.k = b + 2 * up(bq) + up(bl);
         s.v = b + 2 * up(bq) + up(bl) + up(bkv);
+      }
+      char* xb = b + 2 * up(bq) + up(bl) + 2 * up(bkv);
+      for (size_t rb : c->extra_rb) {
+        s.extra.push_back(xb);
+        xb += up(rb * (size_t)chunk_len(c, i) * (size_t)p->batch);
       }
     }
   }
@@ -553,6 +587,7 @@ sppo_status sppo_offload_issue(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* 
     return st;
   }
   if (offload_kv(ctx) && ((st = check_ptr(ctx, src->k, "src.k")) || (st = check_ptr(ctx, src->v, "src.v")))) return st;
+  if ((st = check_extra(ctx, src->extra, "src.extra")) != SPPO_OK) return st;
   const bool fwd_done = ctx->in_bwd || i < ctx->next_fwd;
   if (!fwd_done) return fail(ctx, SPPO_ERR_STATE, "offload of chunk " + std::to_string(i) + " before its forward");
   if (ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " already offloaded");
@@ -564,7 +599,7 @@ sppo_status sppo_offload_issue(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* 
   SPPO_HIP(ctx, hipEventRecord(ctx->t_d2h[i].start, ctx->d2h));
   const int64_t r = ctx->rows[i];
   uint64_t bytes = 0, kv_bytes = 0;
-  SPPO_HIP(ctx, move_qol(ctx, i, r, src->q, src->o, src->lse, true, ctx->d2h, &bytes));
+  SPPO_HIP(ctx, move_qol(ctx, i, r, src->q, src->o, src->lse, src->extra, true, ctx->d2h, &bytes));
   if (offload_kv(ctx)) SPPO_HIP(ctx, move_kv(ctx, i, r, src->k, src->v, true, ctx->d2h, &kv_bytes));
   bytes += kv_bytes;
   SPPO_HIP(ctx, hipEventRecord(ctx->t_d2h[i].stop, ctx->d2h));
@@ -593,6 +628,7 @@ sppo_status sppo_prefetch(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* dst, 
       (st = check_ptr(ctx, dst->lse, "dst.lse"))) {
     return st;
   }
+  if ((st = check_extra(ctx, dst->extra, "dst.extra")) != SPPO_OK) return st;
   if (!ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "prefetch of chunk " + std::to_string(i) + " that was not offloaded");
   if (ctx->prefetched[i]) return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " already prefetched");
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -602,7 +638,7 @@ sppo_status sppo_prefetch(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* dst, 
   SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_off[i], 0));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d[i].start, ctx->h2d));
   uint64_t bytes = 0;
-  SPPO_HIP(ctx, move_qol(ctx, i, ctx->rows[i], dst->q, dst->o, dst->lse, false, ctx->h2d, &bytes));
+  SPPO_HIP(ctx, move_qol(ctx, i, ctx->rows[i], dst->q, dst->o, dst->lse, dst->extra, false, ctx->h2d, &bytes));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d[i].stop, ctx->h2d));
   SPPO_HIP(ctx, hipEventRecord(ctx->ev_pf[i], ctx->h2d));
   ctx->t_h2d[i].pending = true;

@@ -41,4 +41,78 @@ hipError_t launch_bwd_pre_f32(const ChunkArgs& a, hipStream_t stream);
 hipError_t launch_bwd_dkdv_f32(const ChunkArgs& a, hipStream_t stream);
 hipError_t launch_bwd_dq_f32(const ChunkArgs& a, hipStream_t stream);
 
+// Dense bf16 GEMM (fp32 accumulation), C[M, N] (op)= sum_k A(m, k) B(k, n).
+//   tn = 0 (NT): a is [M, K] (row stride lda), b is [N, K] (ldb); K % 64 == 0.
+//   tn = 1 (TN): a is stored [K, M], b is stored [K, N]; M % 256 == 0 and
+//                N % 256 == 0.
+// Rows past M (NT) or K (TN) read as zero; only C[m < M][n < N] is written.
+// Every pointer 16-byte aligned, every leading dimension a multiple of 8.
+enum GemmEpi {
+  kEpiBf16 = 0,     // C bf16 = acc
+  kEpiAddBf16 = 1,  // C bf16 = acc + aux (bf16 [M, N], ldaux): residual
+  kEpiGelu = 2,     // aux bf16 = acc (pre-activation, kept); C bf16 = gelu(bf16(acc))
+  kEpiDGelu = 3,    // C bf16 = acc * gelu'(aux) (aux: the kept pre-activation)
+  kEpiAccF32 = 4,   // C fp32 += acc
+  kEpiF32 = 5       // C fp32 = acc
+};
+struct GemmArgs {
+  int64_t M, N, K;
+  const uint16_t* a;
+  int64_t lda;
+  const uint16_t* b;
+  int64_t ldb;
+  void* c;
+  int64_t ldc;
+  void* aux;
+  int64_t ldaux;
+  int epi;
+  int tn;
+};
+hipError_t launch_gemm_bf16(const GemmArgs& g, hipStream_t stream);
+
+// LayerNorm over rows of H (H % 8 == 0, H <= 8192), bf16 activations, fp32
+// parameters and statistics.  Forward: y, mean, rstd.  Backward: y = dx =
+// dres + LN'(dy), and dgamma/dbeta += the column sums (deterministic: rows
+// in blocks of rows_per_block, partial sums in part [nblocks, 2H], then
+// added in block order).
+struct LnArgs {
+  int64_t rows;
+  int H;
+  const uint16_t* x;
+  int64_t ldx;
+  uint16_t* y;
+  int64_t ldy;
+  const float* gamma;
+  const float* beta;
+  float* mean;
+  float* rstd;
+  float eps;
+  const uint16_t* dy;
+  int64_t lddy;
+  const uint16_t* dres;
+  int64_t lddres;
+  float* dgamma;
+  float* dbeta;
+  float* part;
+  int rows_per_block;
+  int nblocks;
+};
+hipError_t launch_ln_fwd(const LnArgs& a, hipStream_t stream);
+hipError_t launch_ln_bwd(const LnArgs& a, hipStream_t stream);
+hipError_t launch_gelu(const uint16_t* x, uint16_t* y, int64_t n, hipStream_t stream);
+hipError_t launch_transpose(const uint16_t* in, uint16_t* out, int64_t R, int64_t C, hipStream_t stream);
+
+// Rows t < rows of out [rows, wq + 2 wkv] = [dq[t] | bf16(dk[c + t]) |
+// bf16(dv[c + t])] (dq bf16 [rows, wq]; dk, dv fp32 [.., wkv]).
+struct PackArgs {
+  int64_t rows;
+  int wq, wkv;
+  const uint16_t* dq;
+  const float* dk;
+  const float* dv;
+  int64_t c;
+  uint16_t* out;
+};
+hipError_t launch_pack_dqkv(const PackArgs& a, hipStream_t stream);
+
 }  // namespace sppo

@@ -49,6 +49,8 @@ class sppo_problem(ctypes.Structure):
         ("dtype", ctypes.c_int),
         ("softmax_scale", ctypes.c_float),
         ("offload", ctypes.c_int),
+        ("n_extra", ctypes.c_int32),
+        ("extra_row_bytes", ctypes.POINTER(ctypes.c_size_t)),
     ]
 
 
@@ -59,6 +61,7 @@ class sppo_chunk_bufs(ctypes.Structure):
         ("lse", ctypes.c_void_p),
         ("k", ctypes.c_void_p),
         ("v", ctypes.c_void_p),
+        ("extra", ctypes.POINTER(ctypes.c_void_p)),
     ]
 
 
@@ -125,6 +128,17 @@ def lib() -> ctypes.CDLL:
             "sppo_kernel_times": ([P, ctypes.POINTER(sppo_kernel_times_t), I32], ctypes.c_int),
             "sppo_get_offsets": ([P, ctypes.POINTER(ctypes.c_int64), I32], ctypes.c_int),
             "sppo_last_error": ([P], ctypes.c_char_p),
+            "sppo_gemm_bf16": ([I32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, VP, ctypes.c_int64, VP,
+                                ctypes.c_int64, VP, ctypes.c_int64, I32, VP, ctypes.c_int64, VP], ctypes.c_int),
+            "sppo_layernorm_fwd": ([ctypes.c_int64, I32, VP, ctypes.c_int64, VP, VP, ctypes.c_float, VP,
+                                    ctypes.c_int64, VP, VP, VP], ctypes.c_int),
+            "sppo_layernorm_bwd_workspace": ([ctypes.c_int64, I32], ctypes.c_size_t),
+            "sppo_layernorm_bwd": ([ctypes.c_int64, I32, VP, ctypes.c_int64, VP, VP, VP, VP, ctypes.c_int64, VP,
+                                    ctypes.c_int64, VP, ctypes.c_int64, VP, VP, VP, ctypes.c_size_t, VP],
+                                   ctypes.c_int),
+            "sppo_gelu_bf16": ([VP, VP, ctypes.c_int64, VP], ctypes.c_int),
+            "sppo_transpose_bf16": ([VP, VP, ctypes.c_int64, ctypes.c_int64, VP], ctypes.c_int),
+            "sppo_pack_qkv_grad": ([ctypes.c_int64, I32, I32, VP, VP, VP, ctypes.c_int64, VP, VP], ctypes.c_int),
             "sppo_status_string": ([ctypes.c_int], ctypes.c_char_p),
         }
         for name, (args, res) in sig.items():
@@ -204,22 +218,26 @@ def _handle(ctx):
 
 
 def sppo_create(batch, seq_len, n_chunks, n_q_heads, n_kv_heads, head_dim, dtype="bf16",
-                chunk_offsets=None, softmax_scale=0.0, offload="none") -> Ctx:
+                chunk_offsets=None, softmax_scale=0.0, offload="none", extra_row_bytes=()) -> Ctx:
     dt = {"bf16": SPPO_BF16, "f32": SPPO_F32, "fp32": SPPO_F32}.get(dtype, dtype)
     off = OFFLOAD_MODES.get(offload, offload)
     p = sppo_problem(batch, seq_len, n_chunks, None, n_q_heads, n_kv_heads, head_dim, dt,
-                     softmax_scale, off)
+                     softmax_scale, off, len(extra_row_bytes), None)
     arr = None
     if chunk_offsets is not None:
         arr = (ctypes.c_int64 * len(chunk_offsets))(*[int(x) for x in chunk_offsets])
         p.chunk_offsets = arr
+    xrb = None
+    if len(extra_row_bytes):
+        xrb = (ctypes.c_size_t * len(extra_row_bytes))(*[int(x) for x in extra_row_bytes])
+        p.extra_row_bytes = xrb
     out = ctypes.c_void_p()
     st = lib().sppo_create(ctypes.byref(p), ctypes.byref(out))
     if st != SPPO_OK:
         raise SppoError(st, lib().sppo_last_error(None).decode())
     problem = dict(batch=batch, seq_len=seq_len, n_chunks=n_chunks, n_q_heads=n_q_heads,
                    n_kv_heads=n_kv_heads, head_dim=head_dim, dtype=dt, softmax_scale=softmax_scale,
-                   offload=off)
+                   offload=off, extra_row_bytes=tuple(int(x) for x in extra_row_bytes))
     return Ctx(out.value, problem)
 
 
@@ -238,8 +256,13 @@ def sppo_attn_bwd_chunk(ctx, i, q_i, k, v, o_i, lse_i, do_i, dq_i, dk_acc, dv_ac
                                           _ptr(dv_acc), _stream(stream)))
 
 
-def chunk_bufs(q=None, o=None, lse=None, k=None, v=None) -> sppo_chunk_bufs:
-    return sppo_chunk_bufs(_ptr(q), _ptr(o), _ptr(lse), _ptr(k), _ptr(v))
+def chunk_bufs(q=None, o=None, lse=None, k=None, v=None, extra=()) -> sppo_chunk_bufs:
+    b = sppo_chunk_bufs(_ptr(q), _ptr(o), _ptr(lse), _ptr(k), _ptr(v), None)
+    if len(extra):
+        arr = (ctypes.c_void_p * len(extra))(*[_ptr(x) for x in extra])
+        b.extra = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+        b._extra_keepalive = arr  # the array must outlive the struct's use
+    return b
 
 
 def sppo_offload_issue(ctx, i, src: sppo_chunk_bufs, stream=None):
@@ -337,3 +360,48 @@ def sppo_last_error(ctx) -> str:
 
 def sppo_status_string(status: int) -> str:
     return lib().sppo_status_string(status).decode()
+
+
+# ---------------------------------------------------------------- full layer
+SPPO_GEMM_NT, SPPO_GEMM_TN = 0, 1
+EPILOGUES = {"bf16": 0, "add_bf16": 1, "gelu": 2, "dgelu": 3, "acc_f32": 4, "f32": 5}
+
+
+def _plain(status: int):
+    if status != SPPO_OK:
+        raise SppoError(status, status_name(status))
+
+
+def sppo_gemm_bf16(layout, M, N, K, a, lda, b, ldb, c, ldc, epilogue="bf16", aux=None, ldaux=0, stream=None):
+    lay = {"nt": SPPO_GEMM_NT, "tn": SPPO_GEMM_TN}.get(layout, layout)
+    epi = EPILOGUES.get(epilogue, epilogue)
+    _plain(lib().sppo_gemm_bf16(lay, M, N, K, _ptr(a), lda, _ptr(b), ldb, _ptr(c), ldc, epi, _ptr(aux), ldaux,
+                                _stream(stream)))
+
+
+def sppo_layernorm_fwd(rows, H, x, ldx, gamma, beta, eps, y, ldy, mean, rstd, stream=None):
+    _plain(lib().sppo_layernorm_fwd(rows, H, _ptr(x), ldx, _ptr(gamma), _ptr(beta), eps, _ptr(y), ldy, _ptr(mean),
+                                    _ptr(rstd), _stream(stream)))
+
+
+def sppo_layernorm_bwd_workspace(rows, H) -> int:
+    return int(lib().sppo_layernorm_bwd_workspace(rows, H))
+
+
+def sppo_layernorm_bwd(rows, H, x, ldx, gamma, mean, rstd, dy, lddy, dres, lddres, dx, lddx, dgamma, dbeta,
+                       workspace, workspace_bytes, stream=None):
+    _plain(lib().sppo_layernorm_bwd(rows, H, _ptr(x), ldx, _ptr(gamma), _ptr(mean), _ptr(rstd), _ptr(dy), lddy,
+                                    _ptr(dres), lddres, _ptr(dx), lddx, _ptr(dgamma), _ptr(dbeta), _ptr(workspace),
+                                    workspace_bytes, _stream(stream)))
+
+
+def sppo_gelu_bf16(x, y, n, stream=None):
+    _plain(lib().sppo_gelu_bf16(_ptr(x), _ptr(y), n, _stream(stream)))
+
+
+def sppo_transpose_bf16(x, y, rows, cols, stream=None):
+    _plain(lib().sppo_transpose_bf16(_ptr(x), _ptr(y), rows, cols, _stream(stream)))
+
+
+def sppo_pack_qkv_grad(rows, wq, wkv, dq, dk, dv, row0, out, stream=None):
+    _plain(lib().sppo_pack_qkv_grad(rows, wq, wkv, _ptr(dq), _ptr(dk), _ptr(dv), row0, _ptr(out), _stream(stream)))

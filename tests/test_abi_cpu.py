@@ -23,9 +23,10 @@ def test_status_strings():
 
 
 def test_struct_layouts_match_c():
-    # int64, int64, int32(+pad), ptr, int32 x3, enum, float, enum
-    assert ctypes.sizeof(L.sppo_problem) == 56
-    assert ctypes.sizeof(L.sppo_chunk_bufs) == 40
+    # int64, int64, int32(+pad), ptr, int32 x3, enum, float, enum, int32(+pad), ptr
+    assert ctypes.sizeof(L.sppo_problem) == 72
+    assert L.sppo_problem.extra_row_bytes.offset == 64
+    assert ctypes.sizeof(L.sppo_chunk_bufs) == 48
     assert ctypes.sizeof(L.sppo_copy_stats_t) == 40
     assert ctypes.sizeof(L.sppo_link_rates_t) == 24
 
@@ -48,6 +49,8 @@ GOOD = dict(batch=1, seq_len=1024, n_chunks=4, n_q_heads=8, n_kv_heads=2, head_d
     (dict(softmax_scale=float("nan")), L.SPPO_ERR_INVALID_ARG),
     (dict(dtype=7), L.SPPO_ERR_INVALID_ARG),
     (dict(offload=9), L.SPPO_ERR_INVALID_ARG),
+    (dict(extra_row_bytes=[16, 0]), L.SPPO_ERR_INVALID_ARG),      # empty extra plane
+    (dict(extra_row_bytes=[8] * 17), L.SPPO_ERR_INVALID_ARG),     # too many planes
 ])
 def test_create_rejects_invalid_problems(change, status):
     kw = dict(GOOD)
@@ -70,3 +73,27 @@ def test_null_context_is_rejected():
     assert lib.sppo_copy_stats(None, None, 0) == L.SPPO_ERR_INVALID_ARG
     assert lib.sppo_destroy(None) == L.SPPO_OK
     assert lib.sppo_create(None, None) == L.SPPO_ERR_INVALID_ARG
+
+
+def test_layer_ops_reject_invalid_arguments_before_launch():
+    lib = L.lib()
+    a = 4096  # any 16-byte aligned non-null value: nothing is launched on rejection
+    bad = L.SPPO_ERR_INVALID_ARG
+    # NT needs K % 64 == 0; TN needs M, N % 256 == 0; unknown layout/epilogue; misaligned pointers
+    assert lib.sppo_gemm_bf16(0, 128, 256, 100, a, 128, a, 128, a, 256, 0, None, 0, None) == bad
+    assert lib.sppo_gemm_bf16(1, 128, 256, 64, a, 128, a, 256, a, 256, 0, None, 0, None) == bad
+    assert lib.sppo_gemm_bf16(2, 128, 256, 64, a, 64, a, 64, a, 256, 0, None, 0, None) == bad
+    assert lib.sppo_gemm_bf16(0, 128, 256, 64, a, 64, a, 64, a, 256, 9, None, 0, None) == bad
+    assert lib.sppo_gemm_bf16(0, 128, 256, 64, a + 2, 64, a, 64, a, 256, 0, None, 0, None) == bad
+    assert lib.sppo_gemm_bf16(0, 128, 256, 64, a, 64, a, 64, a, 256, 1, None, 0, None) == bad  # ADD needs aux
+    assert lib.sppo_gemm_bf16(0, 0, 256, 64, a, 64, a, 64, a, 256, 0, None, 0, None) == bad
+    # LayerNorm: H % 8, H > 8192, eps <= 0
+    assert lib.sppo_layernorm_fwd(4, 100, a, 100, a, a, 1e-5, a, 100, a, a, None) == bad
+    assert lib.sppo_layernorm_fwd(4, 8200, a, 8200, a, a, 1e-5, a, 8200, a, a, None) == bad
+    assert lib.sppo_layernorm_fwd(4, 64, a, 64, a, a, 0.0, a, 64, a, a, None) == bad
+    ws = lib.sppo_layernorm_bwd_workspace(100, 64)
+    assert ws == 4 * 2 * 64 * 4  # ceil(100 / 32) blocks of [2, H] fp32
+    assert lib.sppo_layernorm_bwd(100, 64, a, 64, a, a, a, a, 64, a, 64, a, 64, a, a, a, ws - 4, None) == bad
+    assert lib.sppo_gelu_bf16(a, a, 12, None) == bad
+    assert lib.sppo_transpose_bf16(a, a, 4, 4, None) == bad          # in place
+    assert lib.sppo_pack_qkv_grad(4, 12, 8, a, a, a, 0, a, None) == bad  # wq % 8

@@ -287,6 +287,12 @@ sppo_status sppo_set_kernel_timing(sppo_ctx* ctx, int32_t enable);
  * counts per kernel since the last reset; `reset_after` != 0 zeroes them. */
 sppo_status sppo_kernel_times(sppo_ctx* ctx, sppo_kernel_times_t* out, int32_t reset_after);
 
+/* The stream waits until chunk i's prefetch (sppo_prefetch) has landed, for
+ * work other than the attention backward (which waits by itself) that
+ * reads the prefetched tensors, e.g. the rest of a layer's backward.
+ * STATE if chunk i's prefetch was not issued. */
+sppo_status sppo_prefetch_wait(sppo_ctx* ctx, int32_t i, void* stream);
+
 /* Chunk offsets as stored by the context (n_chunks + 1 values). */
 sppo_status sppo_get_offsets(const sppo_ctx* ctx, int64_t* out, int32_t capacity);
 
@@ -350,14 +356,16 @@ sppo_status sppo_layernorm_fwd(int64_t rows, int32_t H, const void* x, int64_t l
 /* Backward of the LayerNorm above, with the residual branch folded in:
  *   dx = dres + rstd * (g - mean_j g - xhat * mean_j(g xhat)),
  *   g = dy * gamma, xhat = (x - mean) * rstd,
- * and dgamma += sum_rows dy * xhat, dbeta += sum_rows dy (fp32 [H],
- * accumulated in a fixed order, so results are reproducible bit for bit).
- * workspace: device fp32 scratch of sppo_layernorm_bwd_workspace bytes. */
+ * and dgamma (+)= sum_rows dy * xhat, dbeta (+)= sum_rows dy (fp32 [H];
+ * accumulate != 0 adds, 0 overwrites; the sums run in a fixed order, so
+ * results are reproducible bit for bit).  workspace: device fp32 scratch
+ * of sppo_layernorm_bwd_workspace bytes. */
 size_t sppo_layernorm_bwd_workspace(int64_t rows, int32_t H);
 sppo_status sppo_layernorm_bwd(int64_t rows, int32_t H, const void* x, int64_t ldx, const float* gamma,
                                const float* mean, const float* rstd, const void* dy, int64_t lddy,
                                const void* dres, int64_t lddres, void* dx, int64_t lddx, float* dgamma,
-                               float* dbeta, float* workspace, size_t workspace_bytes, void* stream);
+                               float* dbeta, int32_t accumulate, float* workspace, size_t workspace_bytes,
+                               void* stream);
 
 /* y = gelu(x) (the tanh form above) over n bf16 values, n % 8 == 0. */
 sppo_status sppo_gelu_bf16(const void* x, void* y, int64_t n, void* stream);

@@ -29,3 +29,13 @@ from .causal_attention import (  # noqa: F401
     rows_fwd_bwd,
     tail_keys_bwd,
 )
+from .transformer_layer import (  # noqa: F401
+    chunked_layer,
+    gelu,
+    gelu_grad,
+    layer,
+    layer_backward,
+    layer_forward,
+    layer_norm,
+    layer_norm_bwd,
+)

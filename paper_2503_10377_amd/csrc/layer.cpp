@@ -73,7 +73,8 @@ size_t sppo_layernorm_bwd_workspace(int64_t rows, int32_t H) {
 sppo_status sppo_layernorm_bwd(int64_t rows, int32_t H, const void* x, int64_t ldx, const float* gamma,
                                const float* mean, const float* rstd, const void* dy, int64_t lddy,
                                const void* dres, int64_t lddres, void* dx, int64_t lddx, float* dgamma,
-                               float* dbeta, float* workspace, size_t workspace_bytes, void* stream) {
+                               float* dbeta, int32_t accumulate, float* workspace, size_t workspace_bytes,
+                               void* stream) {
   if (rows <= 0 || H <= 0 || H % 8 || H > 8192) return SPPO_ERR_INVALID_ARG;
   if (ldx < H || lddy < H || lddres < H || lddx < H || ldx % 8 || lddy % 8 || lddres % 8 || lddx % 8)
     return SPPO_ERR_INVALID_ARG;
@@ -91,6 +92,7 @@ sppo_status sppo_layernorm_bwd(int64_t rows, int32_t H, const void* x, int64_t l
   l.dres = static_cast<const uint16_t*>(dres); l.lddres = lddres;
   l.dgamma = dgamma; l.dbeta = dbeta; l.part = workspace;
   l.rows_per_block = kLnRowsPerBlock;
+  l.accumulate = accumulate != 0;
   return launched(sppo::launch_ln_bwd(l, static_cast<hipStream_t>(stream)));
 }
 

@@ -149,7 +149,8 @@ __global__ __launch_bounds__(kLnThreads) void ln_bwd_kernel(LnArgs a) {
   }
 }
 
-// dgamma[c] += sum_b part[b][c], dbeta[c] += sum_b part[b][H + c], in b order.
+// dgamma[c] (+)= sum_b part[b][c], dbeta[c] (+)= sum_b part[b][H + c], in b
+// order.
 __global__ __launch_bounds__(256) void ln_reduce_kernel(LnArgs a) {
   const int c = blockIdx.x * 256 + threadIdx.x;
   if (c >= a.H) return;
@@ -158,8 +159,13 @@ __global__ __launch_bounds__(256) void ln_reduce_kernel(LnArgs a) {
     sg += a.part[(int64_t)b * 2 * a.H + c];
     sb += a.part[(int64_t)b * 2 * a.H + a.H + c];
   }
-  a.dgamma[c] += sg;
-  a.dbeta[c] += sb;
+  if (a.accumulate) {
+    a.dgamma[c] += sg;
+    a.dbeta[c] += sb;
+  } else {
+    a.dgamma[c] = sg;
+    a.dbeta[c] = sb;
+  }
 }
 
 __device__ __forceinline__ float gelu_tanh(float x) {

@@ -648,6 +648,14 @@ sppo_status sppo_prefetch(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* dst, 
   return SPPO_OK;
 }
 
+sppo_status sppo_prefetch_wait(sppo_ctx* ctx, int32_t i, void* stream) {
+  sppo_status st = check_ctx_index(ctx, i);
+  if (st != SPPO_OK) return st;
+  if (!ctx->prefetched[i]) return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " was not prefetched");
+  SPPO_HIP(ctx, hipStreamWaitEvent(static_cast<hipStream_t>(stream), ctx->ev_pf[i], 0));
+  return SPPO_OK;
+}
+
 sppo_status sppo_prefetch_kv(sppo_ctx* ctx, int32_t i, void* k, void* v, void* stream) {
   sppo_status st = check_ctx_index(ctx, i);
   if (st != SPPO_OK) return st;

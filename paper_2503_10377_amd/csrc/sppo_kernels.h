@@ -72,7 +72,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& g, hipStream_t stream);
 
 // LayerNorm over rows of H (H % 8 == 0, H <= 8192), bf16 activations, fp32
 // parameters and statistics.  Forward: y, mean, rstd.  Backward: y = dx =
-// dres + LN'(dy), and dgamma/dbeta += the column sums (deterministic: rows
+// dres + LN'(dy), and dgamma/dbeta (+)= the column sums (deterministic: rows
 // in blocks of rows_per_block, partial sums in part [nblocks, 2H], then
 // added in block order).
 struct LnArgs {
@@ -96,6 +96,7 @@ struct LnArgs {
   float* part;
   int rows_per_block;
   int nblocks;
+  int accumulate;  // bwd: dgamma/dbeta += (1) or = (0) the column sums
 };
 hipError_t launch_ln_fwd(const LnArgs& a, hipStream_t stream);
 hipError_t launch_ln_bwd(const LnArgs& a, hipStream_t stream);

@@ -134,8 +134,9 @@ def lib() -> ctypes.CDLL:
                                     ctypes.c_int64, VP, VP, VP], ctypes.c_int),
             "sppo_layernorm_bwd_workspace": ([ctypes.c_int64, I32], ctypes.c_size_t),
             "sppo_layernorm_bwd": ([ctypes.c_int64, I32, VP, ctypes.c_int64, VP, VP, VP, VP, ctypes.c_int64, VP,
-                                    ctypes.c_int64, VP, ctypes.c_int64, VP, VP, VP, ctypes.c_size_t, VP],
+                                    ctypes.c_int64, VP, ctypes.c_int64, VP, VP, I32, VP, ctypes.c_size_t, VP],
                                    ctypes.c_int),
+            "sppo_prefetch_wait": ([P, I32, VP], ctypes.c_int),
             "sppo_gelu_bf16": ([VP, VP, ctypes.c_int64, VP], ctypes.c_int),
             "sppo_transpose_bf16": ([VP, VP, ctypes.c_int64, ctypes.c_int64, VP], ctypes.c_int),
             "sppo_pack_qkv_grad": ([ctypes.c_int64, I32, I32, VP, VP, VP, ctypes.c_int64, VP, VP], ctypes.c_int),
@@ -389,10 +390,14 @@ def sppo_layernorm_bwd_workspace(rows, H) -> int:
 
 
 def sppo_layernorm_bwd(rows, H, x, ldx, gamma, mean, rstd, dy, lddy, dres, lddres, dx, lddx, dgamma, dbeta,
-                       workspace, workspace_bytes, stream=None):
+                       workspace, workspace_bytes, accumulate=1, stream=None):
     _plain(lib().sppo_layernorm_bwd(rows, H, _ptr(x), ldx, _ptr(gamma), _ptr(mean), _ptr(rstd), _ptr(dy), lddy,
-                                    _ptr(dres), lddres, _ptr(dx), lddx, _ptr(dgamma), _ptr(dbeta), _ptr(workspace),
-                                    workspace_bytes, _stream(stream)))
+                                    _ptr(dres), lddres, _ptr(dx), lddx, _ptr(dgamma), _ptr(dbeta), int(accumulate),
+                                    _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def sppo_prefetch_wait(ctx, i, stream=None):
+    _check(ctx, lib().sppo_prefetch_wait(_handle(ctx), i, _stream(stream)))
 
 
 def sppo_gelu_bf16(x, y, n, stream=None):

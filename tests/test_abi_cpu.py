@@ -71,6 +71,7 @@ def test_null_context_is_rejected():
     assert lib.sppo_reset(None) == L.SPPO_ERR_INVALID_ARG
     assert lib.sppo_sync(None) == L.SPPO_ERR_INVALID_ARG
     assert lib.sppo_copy_stats(None, None, 0) == L.SPPO_ERR_INVALID_ARG
+    assert lib.sppo_prefetch_wait(None, 0, None) == L.SPPO_ERR_INVALID_ARG
     assert lib.sppo_destroy(None) == L.SPPO_OK
     assert lib.sppo_create(None, None) == L.SPPO_ERR_INVALID_ARG
 
@@ -93,7 +94,7 @@ def test_layer_ops_reject_invalid_arguments_before_launch():
     assert lib.sppo_layernorm_fwd(4, 64, a, 64, a, a, 0.0, a, 64, a, a, None) == bad
     ws = lib.sppo_layernorm_bwd_workspace(100, 64)
     assert ws == 4 * 2 * 64 * 4  # ceil(100 / 32) blocks of [2, H] fp32
-    assert lib.sppo_layernorm_bwd(100, 64, a, 64, a, a, a, a, 64, a, 64, a, 64, a, a, a, ws - 4, None) == bad
+    assert lib.sppo_layernorm_bwd(100, 64, a, 64, a, a, a, a, 64, a, 64, a, 64, a, a, 1, a, ws - 4, None) == bad
     assert lib.sppo_gelu_bf16(a, a, 12, None) == bad
     assert lib.sppo_transpose_bf16(a, a, 4, 4, None) == bad          # in place
     assert lib.sppo_pack_qkv_grad(4, 12, 8, a, a, a, 0, a, None) == bad  # wq % 8

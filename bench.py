@@ -177,6 +177,155 @@ def sweep_chunk_count(args, inp, S, Hq, Hkv, D, counts):
         print(json.dumps(row), flush=True)
 
 
+LAYER_WORKLOAD = (131072, 16, 32, 32, 128)  # S, N, Hq, Hkv, D (width 4096, MLP 16384)
+LAYER_METRIC = "full-layer chunked fwd+bwd TFLOP/s (% bf16 MFMA peak) + % offload hidden"
+
+
+def layer_cpu_baseline(inp, p, Hq, Hkv, D, sample_tokens):
+    """Time the fp64 layer oracle (fwd + bwd, unchunked) over the first
+    ``sample_tokens`` tokens of the same inputs and weights."""
+    import numpy as np
+
+    from oracle import transformer_layer as T
+
+    host = lambda t: t.float().cpu().numpy().astype(np.float64)
+    x, dy = host(inp["x"][:sample_tokens]), host(inp["dy"][:sample_tokens])
+    hp = {k: host(v) for k, v in p.items()}
+    try:
+        from threadpoolctl import threadpool_info
+        info = threadpool_info()
+        cores = max(i.get("num_threads", 1) for i in info) if info else 1
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    from paper_2503_10377_amd.chunked_layer import ChunkedLayer
+    flops, _ = ChunkedLayer.flops(sample_tokens, [0, sample_tokens], Hq, Hkv, D)
+    t0 = time.perf_counter()
+    T.layer(x, dy, hp, Hq, Hkv, D)
+    dt = time.perf_counter() - t0
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"fp64 NumPy layer oracle, unchunked fwd+bwd of the full layer over the first "
+                      f"{sample_tokens} tokens ({flops:.3e} algorithmic flop in {dt:.2f} s)"}
+
+
+def layer_bench(args):
+    """One JSON line for the full-layer chunk walk (LayerNorm, QKV / output
+    projections, chunked causal attention, MLP) on the 128K-token workload.
+    The walk with the non-K/V activations offloaded and the same walk
+    without offload are timed in alternating steps (so clock drift over the
+    run falls on both alike); per-op-class times come from events around
+    every library call in one further step of each."""
+    import torch
+
+    from paper_2503_10377_amd import sppo as L
+    from paper_2503_10377_amd.chunked_layer import ChunkedLayer
+    from paper_2503_10377_amd.inputs import make_layer_inputs
+
+    S, N, Hq, Hkv, D = LAYER_WORKLOAD
+    torch.cuda.init()
+    inp, p = make_layer_inputs(S, Hq, Hkv, D, seed=0, device="cuda")
+    st = torch.cuda.current_stream()
+    offload = args.layer_offload
+    print(f"[bench] layer S={S} N={N} Hq={Hq} Hkv={Hkv} D={D} offload={offload}", file=sys.stderr, flush=True)
+    lay = ChunkedLayer(S, N, Hq, Hkv, D, offload=offload)
+    has_copy = lay.offload != L.SPPO_OFFLOAD_NONE
+    lay_off = ChunkedLayer(S, N, Hq, Hkv, D, offload="none") if has_copy and not args.no_offload_compare else None
+    walks = [lay] + ([lay_off] if lay_off else [])
+    out = lay.alloc_outputs()
+    for _ in range(args.warmup):
+        for w in walks:
+            w.step(inp, p, out, lookahead=args.lookahead)
+    torch.cuda.synchronize()
+    if has_copy:
+        L.sppo_copy_stats(lay.ctx, reset_after=True)
+    times = [[] for _ in walks]
+    for n in range(args.steps):
+        for w, t in zip(walks, times):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            w.step(inp, p, out, lookahead=args.lookahead)
+            e1.record(st)
+            t.append((e0, e1))
+    torch.cuda.synchronize()
+    times = [[e0.elapsed_time(e1) for e0, e1 in t] for t in times]
+    cs = L.sppo_copy_stats(lay.ctx, reset_after=True) if has_copy else None
+
+    def breakdown(w):
+        ops, marks = [], []
+        w.step(inp, p, out, lookahead=args.lookahead, ops=ops, marks=marks)
+        torch.cuda.synchronize()
+        cats = {}
+        for cat, flop, e0, e1 in ops:
+            c = cats.setdefault(cat, {"ms": 0.0, "launches": 0, "flop": 0})
+            c["ms"] += e0.elapsed_time(e1)
+            c["launches"] += 1
+            c["flop"] += flop
+        span = {marks[n][0]: marks[n][1].elapsed_time(marks[n + 1][1]) for n in range(len(marks) - 1)}
+        return cats, {"fwd_ms": sum(span[("fwd", i)] for i in range(w.N)),
+                      "bwd_ms": sum(span[("bwd", i)] for i in range(w.N))}
+
+    cats, ph_on = breakdown(lay)
+    total, gemm_flop = ChunkedLayer.flops(S, lay.offsets, Hq, Hkv, D)
+    per_on = sorted(times[0])
+    ms_on = sum(per_on) / len(per_on)
+    tflops = total / (ms_on * 1e-3) / 1e12
+    res = {"metric": LAYER_METRIC, "value": tflops, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms_on, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "pct_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
+           "ms_per_step_median": per_on[len(per_on) // 2], "ms_per_step_min": per_on[0],
+           "ms_steps": [round(t, 2) for t in times[0]],
+           "tokens_per_s": S / (ms_on * 1e-3),
+           "flop_per_step": {"total": total, "gemm": gemm_flop, "attention": total - gemm_flop},
+           "config": {"workload": f"one pre-LayerNorm transformer layer fwd+bwd (width {Hq * D}, MLP {4 * Hq * D}, "
+                                  f"{Hq} query / {Hkv} KV heads x head_dim {D}), batch 1, seq {S} in {N} chunks "
+                                  f"of {S // N}, bf16 in / fp32 accumulate, offload {offload} (all chunks but "
+                                  f"the last), prefetch lookahead {args.lookahead}",
+                      "name": f"layer_s{S // 1024}k_n{N}", "seq_len": S, "n_chunks": N, "n_q_heads": Hq,
+                      "n_kv_heads": Hkv, "head_dim": D, "hidden": Hq * D, "offload": offload}}
+    kern = {}
+    for cat, c in sorted(cats.items()):
+        k = {"ms_per_step": c["ms"], "launches_per_step": c["launches"]}
+        if c["flop"]:
+            k["tflops"] = c["flop"] / (c["ms"] * 1e-3) / 1e12
+        kern[cat] = k
+    g = [c for cat, c in cats.items() if cat.startswith("gemm")]
+    gms, gfl = sum(c["ms"] for c in g), sum(c["flop"] for c in g)
+    kern["gemm_all"] = {"ms_per_step": gms, "launches_per_step": sum(c["launches"] for c in g),
+                        "tflops": gfl / (gms * 1e-3) / 1e12}
+    res["kernels"] = kern
+    res["phases_ms"] = ph_on
+    dom = max((n for n in kern if n != "gemm_all" and "tflops" in kern[n]), key=lambda n: kern[n]["ms_per_step"])
+    ach = kern[dom]["tflops"]
+    res["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
+                       "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": None}
+    if cs is not None:
+        steps = args.steps
+        copy_ms = (cs["ms_d2h"] + cs["ms_h2d"]) / steps
+        off = {"bytes_per_row": lay.offload_bytes_per_row(),
+               "bytes_d2h_per_step": cs["bytes_d2h"] / steps, "bytes_h2d_per_step": cs["bytes_h2d"] / steps,
+               "copy_ms_per_step": copy_ms,
+               "d2h_GBps": cs["bytes_d2h"] / max(cs["ms_d2h"], 1e-9) / 1e6,
+               "h2d_GBps": cs["bytes_h2d"] / max(cs["ms_h2d"], 1e-9) / 1e6}
+        if lay_off is not None:
+            per_off = sorted(times[1])
+            ms_off = sum(per_off) / len(per_off)
+            _, ph_off = breakdown(lay_off)
+            exposed = max(0.0, ms_on - ms_off)
+            off["ms_per_step_no_offload"] = ms_off
+            off["ms_steps_no_offload"] = [round(t, 2) for t in times[1]]
+            off["phases_ms_no_offload"] = ph_off
+            off["exposed_ms_per_step"] = exposed
+            off["hidden_pct"] = 100.0 * max(0.0, min(1.0, 1.0 - exposed / copy_ms)) if copy_ms > 0 else None
+        res["offload"] = off
+        res["offload_hidden_pct"] = off.get("hidden_pct")
+    for w in walks:
+        w.close()
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU layer oracle sample", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = layer_cpu_baseline(inp, p, Hq, Hkv, D, args.layer_cpu_tokens)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -194,6 +343,11 @@ def main():
     ap.add_argument("--sweep-n", default="", metavar="N1,N2,...",
                     help="instead of the headline line: one JSON line per chunk count N at the workload's S and "
                          "heads, no offload (forward and forward+backward time and %% of peak)")
+    ap.add_argument("--layer", action="store_true",
+                    help="instead of the headline line: the full-layer chunk walk (projections, attention, MLP) "
+                         "at seq 131072 in 16 chunks, width 4096")
+    ap.add_argument("--layer-offload", default="qol", choices=("none", "qol", "qkvol"))
+    ap.add_argument("--layer-cpu-tokens", type=int, default=4096)
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -202,6 +356,10 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the sharded path is "
               "described, not built.", file=sys.stderr)
         sys.exit(2)
+
+    if args.layer:
+        layer_bench(args)
+        return
 
     import torch
 

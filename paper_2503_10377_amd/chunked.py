@@ -19,17 +19,21 @@ K/V cache rows of the offloaded chunks are given up once the forward walk is
 over; their copies are queued on the host-to-device stream right before the
 backward of the last chunk, whose dK/dV work consumes them chunk by chunk in
 the order they arrive.
+
+Host pacing: the host stays at most ``host_ahead`` chunk boundaries ahead of
+the device (a HostPacer; 0 lets it run free).
 """
 from __future__ import annotations
 
 import torch
 
 from . import sppo as L
+from .pacing import HostPacer
 
 
 class ChunkedAttention:
     def __init__(self, B, S, n_chunks, Hq, Hkv, D, dtype="bf16", offsets=None, scale=0.0,
-                 offload="none", device="cuda"):
+                 offload="none", device="cuda", host_ahead=2):
         self.ctx = L.sppo_create(B, S, n_chunks, Hq, Hkv, D, dtype=dtype, chunk_offsets=offsets,
                                  softmax_scale=scale, offload=offload)
         self.B, self.S, self.N, self.Hq, self.Hkv, self.D = B, S, n_chunks, Hq, Hkv, D
@@ -37,6 +41,7 @@ class ChunkedAttention:
         self.torch_dtype = torch.bfloat16 if self.ctx.problem["dtype"] == L.SPPO_BF16 else torch.float32
         self.offload = L.OFFLOAD_MODES.get(offload, offload)
         self.device = device
+        self.pacer = HostPacer(host_ahead)
 
     def close(self):
         self.ctx.close()
@@ -116,6 +121,7 @@ class ChunkedAttention:
         rows = self.offload_rows() if poison else None
 
         def mark(label):
+            self.pacer.boundary(s)
             if marks is not None:
                 e = torch.cuda.Event(enable_timing=True)
                 e.record(s)

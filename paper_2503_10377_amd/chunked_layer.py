@@ -17,6 +17,9 @@ LayerNorms' statistics -- is offloaded after the chunk's forward (all chunks
 but the last by default) and prefetched before its backward.  u, z and
 gelu(a) are recomputed in the backward from x, h and a.
 
+The host stays at most ``host_ahead`` chunk boundaries ahead of the device
+(a HostPacer; 0 lets it run free).
+
 Only C-ABI calls and torch allocations happen here; every arithmetic step
 runs in the library's kernels.
 """
@@ -25,12 +28,14 @@ from __future__ import annotations
 import torch
 
 from . import sppo as L
+from .pacing import HostPacer
 
 PLANES = ("x", "h", "a", "m1", "r1", "m2", "r2")
 
 
 class ChunkedLayer:
-    def __init__(self, S, n_chunks, Hq, Hkv, D, offsets=None, offload="none", device="cuda", eps=1e-5):
+    def __init__(self, S, n_chunks, Hq, Hkv, D, offsets=None, offload="none", device="cuda", eps=1e-5,
+                 host_ahead=2):
         H = Hq * D
         wt = (Hq + 2 * Hkv) * D
         if H % 256 or wt % 256 or H > 8192:
@@ -44,6 +49,7 @@ class ChunkedLayer:
         self.offsets = L.sppo_get_offsets(self.ctx)
         self.offload = L.OFFLOAD_MODES.get(offload, offload)
         self.s_max = max(self.offsets[i + 1] - self.offsets[i] for i in range(n_chunks))
+        self.pacer = HostPacer(host_ahead)
         self._alloc()
 
     def close(self):
@@ -117,12 +123,16 @@ class ChunkedLayer:
         return L.chunk_bufs(q=v["q"], o=v["o"], lse=v["lse"], k=self.k, v=self.v,
                             extra=[v[name] for name in PLANES])
 
-    def step(self, inp, p, out, offload_chunks=None, lookahead=2, poison=False, stream=None, marks=None):
+    def step(self, inp, p, out, offload_chunks=None, lookahead=2, poison=False, stream=None, marks=None,
+             ops=None):
         """Forward and backward of the layer over all chunks.  inp: x, dy
         [S, H] bf16 (x's chunk rows are the x planes: offloading a chunk
         makes its rows of x dead until the prefetch; poison=True overwrites
         them, and every other offloaded row, with NaN once copied).  p: the
-        weights (w_qkv, w_o, w_1, w_2 bf16; g1, b1, g2, b2 fp32)."""
+        weights (w_qkv, w_o, w_1, w_2 bf16; g1, b1, g2, b2 fp32).  marks:
+        list that receives ((phase, chunk), event) at every chunk boundary.
+        ops: list that receives (category, algorithmic flop, start event,
+        end event) around every library call on the compute stream."""
         s = torch.cuda.current_stream() if stream is None else stream
         H, Wt, HqD, HkvD = self.H, self.Wt, self.Hq * self.D, self.Hkv * self.D
         if offload_chunks is None:
@@ -132,29 +142,54 @@ class ChunkedLayer:
         x, dy = inp["x"], inp["dy"]
 
         def mark(label):
+            self.pacer.boundary(s)
             if marks is not None:
                 ev = torch.cuda.Event(enable_timing=True)
                 ev.record(s)
                 marks.append((label, ev))
 
+        def timed(cat, fn, flop=0):
+            def call(*a, **kw):
+                if ops is None:
+                    return fn(*a, **kw)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(s)
+                r = fn(*a, **kw)
+                e1.record(s)
+                ops.append((cat(a) if callable(cat) else cat, flop(a) if callable(flop) else flop, e0, e1))
+                return r
+            return call
+
+        gemm = timed(lambda a: "gemm_" + a[0] + ("_fwd" if fwd_phase[0] and a[0] == "nt" else
+                                                 "_bwd" if a[0] == "nt" else ""),
+                     L.sppo_gemm_bf16, lambda a: 2 * a[1] * a[2] * a[3])
+        fwd_phase = [True]
+        transpose = timed("transpose", L.sppo_transpose_bf16)
+        ln_fwd = timed("layernorm", L.sppo_layernorm_fwd)
+        ln_bwd = timed("layernorm", L.sppo_layernorm_bwd)
+        gelu = timed("gelu", L.sppo_gelu_bf16)
+        pack = timed("pack", L.sppo_pack_qkv_grad)
+        pairs = lambda a: self.chunk_len(a[1]) * self.offsets[a[1]] + self.chunk_len(a[1]) * (self.chunk_len(a[1]) + 1) // 2
+        attn_fwd = timed("attn_fwd", L.sppo_attn_fwd_chunk, lambda a: 4 * self.D * self.Hq * pairs(a))
+        attn_bwd = timed("attn_bwd", L.sppo_attn_bwd_chunk, lambda a: 10 * self.D * self.Hq * pairs(a))
+
         mark(("wT", -1))
-        L.sppo_transpose_bf16(p["w_qkv"], self.wT["w_qkv"], H, Wt, s)
-        L.sppo_transpose_bf16(p["w_o"], self.wT["w_o"], HqD, H, s)
-        L.sppo_transpose_bf16(p["w_1"], self.wT["w_1"], H, 4 * H, s)
-        L.sppo_transpose_bf16(p["w_2"], self.wT["w_2"], 4 * H, H, s)
-        gemm = L.sppo_gemm_bf16
+        transpose(p["w_qkv"], self.wT["w_qkv"], H, Wt, s)
+        transpose(p["w_o"], self.wT["w_o"], HqD, H, s)
+        transpose(p["w_1"], self.wT["w_1"], H, 4 * H, s)
+        transpose(p["w_2"], self.wT["w_2"], 4 * H, H, s)
         for i in range(self.N):
             mark(("fwd", i))
             n, c0, v = self.chunk_len(i), self.offsets[i], self._views(x, i)
             u, z, g = self.u[:n], self.z[:n], self.g[:n]
-            L.sppo_layernorm_fwd(n, H, v["x"], H, p["g1"], p["b1"], self.eps, u, H, v["m1"], v["r1"], s)
+            ln_fwd(n, H, v["x"], H, p["g1"], p["b1"], self.eps, u, H, v["m1"], v["r1"], s)
             wq = self.wT["w_qkv"]
             gemm("nt", n, HqD, H, u, H, wq, H, v["q"], HqD, stream=s)
             gemm("nt", n, HkvD, H, u, H, wq[HqD:], H, self.k[c0:], HkvD, stream=s)
             gemm("nt", n, HkvD, H, u, H, wq[HqD + HkvD:], H, self.v[c0:], HkvD, stream=s)
-            L.sppo_attn_fwd_chunk(self.ctx, i, v["q"], self.k, self.v, v["o"], v["lse"], s)
+            attn_fwd(self.ctx, i, v["q"], self.k, self.v, v["o"], v["lse"], s)
             gemm("nt", n, H, HqD, v["o"], HqD, self.wT["w_o"], HqD, v["h"], H, "add_bf16", v["x"], H, stream=s)
-            L.sppo_layernorm_fwd(n, H, v["h"], H, p["g2"], p["b2"], self.eps, z, H, v["m2"], v["r2"], s)
+            ln_fwd(n, H, v["h"], H, p["g2"], p["b2"], self.eps, z, H, v["m2"], v["r2"], s)
             gemm("nt", n, 4 * H, H, z, H, self.wT["w_1"], H, g, 4 * H, "gelu", v["a"], 4 * H, stream=s)
             gemm("nt", n, H, 4 * H, g, 4 * H, self.wT["w_2"], 4 * H, out["y"][c0:], H, "add_bf16", v["h"], H,
                  stream=s)
@@ -168,6 +203,7 @@ class ChunkedLayer:
                         for name in ("x", "q", "o", "h", "a", "m1", "r1", "m2", "r2"):
                             v[name][:r].fill_(float("nan"))
                         v["lse"][:, :r].fill_(float("nan"))
+        fwd_phase[0] = False
         pending = sorted(offl, reverse=True)
         nxt = 0
         for i in reversed(range(self.N)):
@@ -185,28 +221,28 @@ class ChunkedLayer:
             da, dz, dh, dO = self.da[:n], self.dz[:n], self.dh[:n], self.dO[:n]
             dyi = dy[c0:c0 + n]
             # y = h + gelu(a) W2
-            L.sppo_gelu_bf16(v["a"], g, n * 4 * H, s)
+            gelu(v["a"], g, n * 4 * H, s)
             gemm("nt", n, 4 * H, H, dyi, H, p["w_2"], H, da, 4 * H, "dgelu", v["a"], 4 * H, stream=s)
             gemm("tn", 4 * H, H, n, g, 4 * H, dyi, H, out["dw_2"], H, wacc, stream=s)
             # a = z W1, z = LN2(h)
-            L.sppo_layernorm_fwd(n, H, v["h"], H, p["g2"], p["b2"], self.eps, z, H, v["m2"], v["r2"], s)
+            ln_fwd(n, H, v["h"], H, p["g2"], p["b2"], self.eps, z, H, v["m2"], v["r2"], s)
             gemm("nt", n, H, 4 * H, da, 4 * H, p["w_1"], 4 * H, dz, H, stream=s)
             gemm("tn", H, 4 * H, n, z, H, da, 4 * H, out["dw_1"], 4 * H, wacc, stream=s)
-            L.sppo_layernorm_bwd(n, H, v["h"], H, p["g2"], v["m2"], v["r2"], dz, H, dyi, H, dh, H, out["dg2"],
+            ln_bwd(n, H, v["h"], H, p["g2"], v["m2"], v["r2"], dz, H, dyi, H, dh, H, out["dg2"],
                                  out["db2"], self.ws, self.ws_bytes, accumulate=0 if first else 1, stream=s)
             # h = x + O Wo
             gemm("nt", n, HqD, H, dh, H, p["w_o"], H, dO, HqD, stream=s)
             gemm("tn", HqD, H, n, v["o"], HqD, dh, H, out["dw_o"], H, wacc, stream=s)
-            L.sppo_attn_bwd_chunk(self.ctx, i, v["q"], self.k, self.v, v["o"], v["lse"], dO, self.dq[:n],
+            attn_bwd(self.ctx, i, v["q"], self.k, self.v, v["o"], v["lse"], dO, self.dq[:n],
                                   self.dk, self.dv, s)
             # q, k, v = u W_qkv (chunk i's dK/dV rows are complete now)
             dqkv = self.dqkv[:n]
-            L.sppo_pack_qkv_grad(n, HqD, HkvD, self.dq[:n], self.dk, self.dv, c0, dqkv, s)
-            L.sppo_layernorm_fwd(n, H, v["x"], H, p["g1"], p["b1"], self.eps, u, H, v["m1"], v["r1"], s)
+            pack(n, HqD, HkvD, self.dq[:n], self.dk, self.dv, c0, dqkv, s)
+            ln_fwd(n, H, v["x"], H, p["g1"], p["b1"], self.eps, u, H, v["m1"], v["r1"], s)
             gemm("nt", n, H, Wt, dqkv, Wt, p["w_qkv"], Wt, self.du[:n], H, stream=s)
             gemm("tn", H, Wt, n, u, H, dqkv, Wt, out["dw_qkv"], Wt, wacc, stream=s)
             # u = LN1(x); x also reaches h
-            L.sppo_layernorm_bwd(n, H, v["x"], H, p["g1"], v["m1"], v["r1"], self.du[:n], H, dh, H,
+            ln_bwd(n, H, v["x"], H, p["g1"], v["m1"], v["r1"], self.du[:n], H, dh, H,
                                  out["dx"][c0:], H, out["dg1"], out["db1"], self.ws, self.ws_bytes,
                                  accumulate=0 if first else 1, stream=s)
         mark(("end", -1))

@@ -63,3 +63,33 @@ def make_inputs(B: int, S: int, Hq: int, Hkv: int, D: int, dtype=torch.bfloat16,
             src = torch.cat([k[:, 1:], k[:, -1:]], dim=1)
         q = (2 * src).repeat_interleave(G, dim=2).contiguous()
     return {"q": q, "k": k, "v": v, "do": do}
+
+
+LAYER_IDS = {"x": 0, "dy": 1, "w_qkv": 2, "w_o": 3, "w_1": 4, "w_2": 5, "g1": 6, "b1": 7, "g2": 8, "b2": 9}
+
+
+def make_layer_inputs(S: int, Hq: int, Hkv: int, D: int, seed: int = 0, device="cuda"):
+    """Inputs and parameters of one pre-LayerNorm transformer layer of width
+    H = Hq*D: x, dy [S, H] ~ N(0, 1) in bf16; weights [in, out] ~ N(0, 1/in)
+    in bf16 (w_qkv [H, (Hq+2Hkv)D], w_o [Hq D, H], w_1 [H, 4H], w_2 [4H, H]);
+    LayerNorm gamma ~ 1 + 0.1 N(0, 1), beta ~ 0.1 N(0, 1) in fp32.  Each
+    tensor has its own seed derived from (seed, tensor)."""
+    H, wt = Hq * D, (Hq + 2 * Hkv) * D
+    shapes = {"x": (S, H), "dy": (S, H), "w_qkv": (H, wt), "w_o": (Hq * D, H), "w_1": (H, 4 * H),
+              "w_2": (4 * H, H), "g1": (H,), "b1": (H,), "g2": (H,), "b2": (H,)}
+    gen = torch.Generator(device=device)
+    out = {}
+    for name, shape in shapes.items():
+        gen.manual_seed(_block_seed(seed, 8 + LAYER_IDS[name], 0, 0))
+        t = torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+        if name.startswith("w_"):
+            out[name] = (t * shape[0] ** -0.5).to(torch.bfloat16)
+        elif name in ("g1", "g2"):
+            out[name] = 1.0 + 0.1 * t
+        elif name in ("b1", "b2"):
+            out[name] = 0.1 * t
+        else:
+            out[name] = t.to(torch.bfloat16)
+        del t
+    inp = {k: out.pop(k) for k in ("x", "dy")}
+    return inp, out

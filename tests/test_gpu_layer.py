@@ -22,6 +22,7 @@ import torch
 from oracle import transformer_layer as T
 from paper_2503_10377_amd import sppo as L
 from paper_2503_10377_amd.chunked_layer import ChunkedLayer
+from paper_2503_10377_amd.inputs import make_layer_inputs
 from parity import to_np
 
 pytestmark = pytest.mark.gpu
@@ -34,24 +35,10 @@ def announce(msg):
     print(f"\n[case] {msg}", file=sys.stderr, flush=True)
 
 
-def make_layer_inputs(S, Hq, Hkv, D, seed):
-    """x, dy ~ N(0, 1); weights ~ N(0, 1/fan_in); LayerNorm gamma ~ 1 + 0.1 N,
-    beta ~ 0.1 N (a seeded CPU generator; nothing here is GPU output)."""
-    H, wt = Hq * D, (Hq + 2 * Hkv) * D
-    g = torch.Generator().manual_seed(seed)
-    r = lambda *shape, s=1.0: torch.randn(*shape, generator=g) * s
-    bf = torch.bfloat16
-    p = {"w_qkv": r(H, wt, s=H ** -0.5).to(bf), "w_o": r(Hq * D, H, s=(Hq * D) ** -0.5).to(bf),
-         "w_1": r(H, 4 * H, s=H ** -0.5).to(bf), "w_2": r(4 * H, H, s=(4 * H) ** -0.5).to(bf),
-         "g1": 1 + r(H, s=0.1), "b1": r(H, s=0.1), "g2": 1 + r(H, s=0.1), "b2": r(H, s=0.1)}
-    inp = {"x": r(S, H).to(bf), "dy": r(S, H).to(bf)}
-    return inp, p
-
-
 def run_layer(S, Hq, Hkv, D, offsets, seed=0, offload="none", poison=False, lookahead=2, rows=None):
     announce(f"layer S={S} Hq={Hq} Hkv={Hkv} D={D} offsets={offsets} seed={seed} offload={offload} "
              f"poison={poison} rows={rows}")
-    inp, p = make_layer_inputs(S, Hq, Hkv, D, seed)
+    inp, p = make_layer_inputs(S, Hq, Hkv, D, seed, device="cpu")
     host = {k: to_np(v) for k, v in {**inp, **p}.items()}
     dinp = {k: v.cuda() for k, v in inp.items()}
     dp = {k: v.cuda() for k, v in p.items()}

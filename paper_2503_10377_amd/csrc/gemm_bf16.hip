@@ -25,16 +25,6 @@ constexpr int GBM = 256, GBN = 256, GBK = 64;
 
 __device__ __forceinline__ float bf16_round(float x) { return (float)(__bf16)x; }
 
-// GELU, tanh form: 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))).
-__device__ __forceinline__ float gelu_tanh(float x) {
-  const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
-  return 0.5f * x * (1.f + tanhf(u));
-}
-__device__ __forceinline__ float gelu_tanh_grad(float x) {
-  const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
-  const float t = tanhf(u);
-  return 0.5f * (1.f + t) + 0.5f * x * (1.f - t * t) * 0.7978845608028654f * (1.f + 3.f * 0.044715f * x * x);
-}
 
 template <int TN, int EPI>
 __global__ __launch_bounds__(512, 1) void gemm_bf16_kernel(GemmArgs g) {

@@ -168,11 +168,6 @@ __global__ __launch_bounds__(256) void ln_reduce_kernel(LnArgs a) {
   }
 }
 
-__device__ __forceinline__ float gelu_tanh(float x) {
-  const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
-  return 0.5f * x * (1.f + tanhf(u));
-}
-
 // y = gelu(x) elementwise over n bf16 values (n % 8 == 0).
 __global__ __launch_bounds__(256) void gelu_kernel(const uint16_t* x, uint16_t* y, int64_t n) {
   const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;

@@ -225,4 +225,17 @@ __device__ __forceinline__ bf16x8 ld_tr(const uint16_t* X, int lo, int hi) {
   return as_bf16x8(u32x4{a2.x, a2.y, b2.x, b2.y});
 }
 
+// GELU in its tanh form, x/2 (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))), and
+// its derivative; shared by the GEMM epilogues and the recompute kernel so
+// the forward and the backward evaluate the same expression.
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
+  return 0.5f * x * (1.f + tanhf(u));
+}
+__device__ __forceinline__ float gelu_tanh_grad(float x) {
+  const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
+  const float t = tanhf(u);
+  return 0.5f * (1.f + t) + 0.5f * x * (1.f - t * t) * 0.7978845608028654f * (1.f + 3.f * 0.044715f * x * x);
+}
+
 }  // namespace sppo

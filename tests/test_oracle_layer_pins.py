@@ -120,3 +120,58 @@ def test_chunked_walk_equals_unchunked_layer(offsets):
     got = T.chunked_layer(x, dy, p, hq, hkv, d, offsets)
     for key, val in ref.items():
         np.testing.assert_allclose(got[key], val, rtol=1e-10, atol=1e-11, err_msg=key)
+
+
+def test_gelu_tanh_form_is_within_its_error_of_the_exact_gelu():
+    # The tanh form approximates x Phi(x) to within 4.8e-4 everywhere; a wrong
+    # constant (0.04715 for 0.044715, or sqrt(1/pi)) is off by 1e-3 or more.
+    a = np.linspace(-8, 8, 20001)
+    exact = a * 0.5 * (1 + np.array([math.erf(v / math.sqrt(2)) for v in a]))
+    err = np.abs(T.gelu(a) - exact)
+    assert err.max() < 4.8e-4
+    assert err.max() > 4.6e-4  # the approximation's own error, not a fit to the exact one
+
+
+def test_layer_norm_matches_torch():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(5)
+    x = rng.normal(1.0, 3.0, (9, 24))
+    g, b = rng.normal(1, 0.2, 24), rng.normal(0, 0.2, 24)
+    y, mean, rstd = T.layer_norm(x, g, b)
+    ref = torch.nn.functional.layer_norm(torch.tensor(x), (24,), torch.tensor(g), torch.tensor(b), eps=T.EPS)
+    np.testing.assert_allclose(y, ref.numpy(), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2)])
+def test_layer_matches_torch_autograd(hq, hkv):
+    # The pre-LayerNorm GPT block built from torch's own LayerNorm, tanh GELU
+    # and causal scaled-dot-product attention in fp64, differentiated by
+    # autograd: an implementation and a gradient derived independently of
+    # the oracle's hand-written chain rule.
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
+    rng = np.random.default_rng(6)
+    d, S = 4, 11
+    h = hq * d
+    p = params(rng, h=h, hq=hq, hkv=hkv, d=d)
+    x, dy = rng.normal(size=(S, h)), rng.normal(size=(S, h))
+    tp = {k: torch.tensor(v, requires_grad=True) for k, v in p.items()}
+    tx = torch.tensor(x, requires_grad=True)
+    u = F.layer_norm(tx, (h,), tp["g1"], tp["b1"], eps=T.EPS)
+    qkv = u @ tp["w_qkv"]
+    q = qkv[:, :hq * d].reshape(S, hq, d).transpose(0, 1)
+    k = qkv[:, hq * d:(hq + hkv) * d].reshape(S, hkv, d).transpose(0, 1)
+    v = qkv[:, (hq + hkv) * d:].reshape(S, hkv, d).transpose(0, 1)
+    k, v = k.repeat_interleave(hq // hkv, dim=0), v.repeat_interleave(hq // hkv, dim=0)
+    o = F.scaled_dot_product_attention(q[None], k[None], v[None], is_causal=True)[0]
+    hh = tx + o.transpose(0, 1).reshape(S, hq * d) @ tp["w_o"]
+    z = F.layer_norm(hh, (h,), tp["g2"], tp["b2"], eps=T.EPS)
+    y = hh + F.gelu(z @ tp["w_1"], approximate="tanh") @ tp["w_2"]
+    (y * torch.tensor(dy)).sum().backward()
+    got = T.layer(x, dy, p, hq, hkv, d)
+    np.testing.assert_allclose(got["y"], y.detach().numpy(), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(got["dx"], tx.grad.numpy(), rtol=1e-10, atol=1e-11)
+    for name in ("w_qkv", "w_o", "w_1", "w_2"):
+        np.testing.assert_allclose(got["d" + name], tp[name].grad.numpy(), rtol=1e-10, atol=1e-11, err_msg=name)
+    for name, key in (("g1", "dg1"), ("b1", "db1"), ("g2", "dg2"), ("b2", "db2")):
+        np.testing.assert_allclose(got[key], tp[name].grad.numpy(), rtol=1e-10, atol=1e-11, err_msg=name)

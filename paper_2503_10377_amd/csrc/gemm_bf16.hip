@@ -122,20 +122,28 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_kernel(GemmArgs g) {
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = f32x16{};
   }
-  // Four k-steps per stage, each six operand reads then eight MFMAs; the
-  // second wave on the SIMD covers the read latency.
+  // Four k-steps per stage, eight MFMAs each; the six operand reads of k-step
+  // kk+1 are issued before the MFMAs of k-step kk (register double buffer),
+  // and the second wave on the SIMD covers what latency remains.
   auto compute = [&](const uint16_t* sa, const uint16_t* sb) {
+    bf16x8 ao[2][2], bo[2][4];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) ao[0][mt] = a_op(sa, mt, 0);
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) bo[0][nt] = b_op(sb, nt, 0);
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      bf16x8 ao[2], bo[4];
+      const int cur = kk & 1, nxt = cur ^ 1;
+      if (kk < 3) {
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) ao[mt] = a_op(sa, mt, kk);
+        for (int mt = 0; mt < 2; ++mt) ao[nxt][mt] = a_op(sa, mt, kk + 1);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) bo[nt] = b_op(sb, nt, kk);
+        for (int nt = 0; nt < 4; ++nt) bo[nxt][nt] = b_op(sb, nt, kk + 1);
+      }
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = mfma32(ao[mt], bo[nt], acc[mt][nt]);
+        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = mfma32(ao[cur][mt], bo[cur][nt], acc[mt][nt]);
       }
       __builtin_amdgcn_sched_barrier(0);
     }

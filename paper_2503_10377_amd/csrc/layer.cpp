@@ -14,7 +14,7 @@ bool al16(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 sppo_status launched(hipError_t e) { return e == hipSuccess ? SPPO_OK : SPPO_ERR_HIP; }
 
-constexpr int kLnRowsPerBlock = 32;
+constexpr int kLnRowsPerBlock = 16;
 
 }  // namespace
 

@@ -83,61 +83,98 @@ __global__ __launch_bounds__(kLnThreads) void ln_fwd_kernel(LnArgs a) {
   }
 }
 
+// N block-wide sums at once (four waves): one shuffle tree per value, one
+// round through LDS.
+template <int N>
+__device__ __forceinline__ void block_sum_n(float (&v)[N], float* red) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v[i] += __shfl_xor(v[i], off);
+  }
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __syncthreads();  // red may still be read by a previous reduction
+  if (lane == 0) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) red[w * N + i] = v[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = red[i] + red[N + i] + red[2 * N + i] + red[3 * N + i];
+}
+
 // Backward of y = xhat * gamma + beta, xhat = (x - mean) * rstd, per row:
 //   dx = dres + rstd * (g - mean_j(g) - xhat * mean_j(g * xhat)),  g = dy * gamma
 // (dres: the gradient that reaches x around the LayerNorm, the residual
-// branch).  Workgroup b handles rows [b R, b R + R) and writes its partial
-// sums of dy * xhat and dy over those rows (the gamma and beta gradients) to
-// part[b]; ln_reduce adds the partials in block order.
+// branch).  Workgroup b handles rows [b R, b R + R), two rows at a time (one
+// reduction for both), and writes its partial sums of dy * xhat and dy over
+// those rows (the gamma and beta gradients) to part[b]; ln_reduce adds the
+// partials.  PER 16-byte column groups per thread (H <= 2048 PER).
+template <int PER>
 __global__ __launch_bounds__(kLnThreads) void ln_bwd_kernel(LnArgs a) {
-  __shared__ float red[4];
+  __shared__ float red[4 * 4];
   const int H = a.H, tid = threadIdx.x;
   const int64_t r0 = (int64_t)blockIdx.x * a.rows_per_block;
   const int64_t r1 = r0 + a.rows_per_block < a.rows ? r0 + a.rows_per_block : a.rows;
-  float pg[kLnMaxPer][8], pb[kLnMaxPer][8];
+  float pg[PER][8], pb[PER][8];
 #pragma unroll
-  for (int p = 0; p < kLnMaxPer; ++p) {
+  for (int p = 0; p < PER; ++p) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) pg[p][e] = pb[p][e] = 0.f;
   }
-  for (int64_t row = r0; row < r1; ++row) {
-    const float mean = a.mean[row], rstd = a.rstd[row];
-    float xh[kLnMaxPer][8], gg[kLnMaxPer][8];
-    float s1 = 0.f, s2 = 0.f;
+  for (int64_t row = r0; row < r1; row += 2) {
+    const bool two = row + 1 < r1;
+    float xh[2][PER][8], gg[2][PER][8];
+    float sums[4] = {0.f, 0.f, 0.f, 0.f};
+    float mean[2], rstd[2];
 #pragma unroll
-    for (int p = 0; p < kLnMaxPer; ++p) {
-      const int c = 8 * (tid + kLnThreads * p);
-      if (c < H) {
-        float xv[8], dv[8];
-        unpack8(ld_global16(a.x + row * a.ldx + c), xv);
-        unpack8(ld_global16(a.dy + row * a.lddy + c), dv);
+    for (int j = 0; j < 2; ++j) {
+      const int64_t rr = j == 0 || two ? row + j : row;  // a lone last row is read twice, used once
+      mean[j] = a.mean[rr];
+      rstd[j] = a.rstd[rr];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          xh[p][e] = (xv[e] - mean) * rstd;
-          gg[p][e] = dv[e] * a.gamma[c + e];
-          s1 += gg[p][e];
-          s2 += gg[p][e] * xh[p][e];
-          pg[p][e] += dv[e] * xh[p][e];
-          pb[p][e] += dv[e];
+      for (int p = 0; p < PER; ++p) {
+        const int c = 8 * (tid + kLnThreads * p);
+        if (c < H) {
+          float xv[8], dv[8];
+          unpack8(ld_global16(a.x + rr * a.ldx + c), xv);
+          unpack8(ld_global16(a.dy + rr * a.lddy + c), dv);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            xh[j][p][e] = (xv[e] - mean[j]) * rstd[j];
+            gg[j][p][e] = dv[e] * a.gamma[c + e];
+            sums[2 * j] += gg[j][p][e];
+            sums[2 * j + 1] += gg[j][p][e] * xh[j][p][e];
+            if (j == 0 || two) {
+              pg[p][e] += dv[e] * xh[j][p][e];
+              pb[p][e] += dv[e];
+            }
+          }
         }
       }
     }
-    const float m1 = block_sum(s1, red) / H, m2 = block_sum(s2, red) / H;
+    block_sum_n<4>(sums, red);
 #pragma unroll
-    for (int p = 0; p < kLnMaxPer; ++p) {
-      const int c = 8 * (tid + kLnThreads * p);
-      if (c < H) {
-        float rv[8], o[8];
-        unpack8(ld_global16(a.dres + row * a.lddres + c), rv);
+    for (int j = 0; j < 2; ++j) {
+      if (j == 1 && !two) break;
+      const int64_t rr = row + j;
+      const float m1 = sums[2 * j] / H, m2 = sums[2 * j + 1] / H;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = rv[e] + rstd * (gg[p][e] - m1 - xh[p][e] * m2);
-        *reinterpret_cast<u32x4*>(a.y + row * a.ldy + c) = pack8(o);
+      for (int p = 0; p < PER; ++p) {
+        const int c = 8 * (tid + kLnThreads * p);
+        if (c < H) {
+          float rv[8], o[8];
+          unpack8(ld_global16(a.dres + rr * a.lddres + c), rv);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = rv[e] + rstd[j] * (gg[j][p][e] - m1 - xh[j][p][e] * m2);
+          *reinterpret_cast<u32x4*>(a.y + rr * a.ldy + c) = pack8(o);
+        }
       }
     }
   }
   float* part = a.part + (int64_t)blockIdx.x * 2 * H;
 #pragma unroll
-  for (int p = 0; p < kLnMaxPer; ++p) {
+  for (int p = 0; p < PER; ++p) {
     const int c = 8 * (tid + kLnThreads * p);
     if (c < H) {
 #pragma unroll
@@ -149,22 +186,29 @@ __global__ __launch_bounds__(kLnThreads) void ln_bwd_kernel(LnArgs a) {
   }
 }
 
-// dgamma[c] (+)= sum_b part[b][c], dbeta[c] (+)= sum_b part[b][H + c], in b
-// order.
-__global__ __launch_bounds__(256) void ln_reduce_kernel(LnArgs a) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= a.H) return;
-  float sg = 0.f, sb = 0.f;
-  for (int b = 0; b < a.nblocks; ++b) {
-    sg += a.part[(int64_t)b * 2 * a.H + c];
-    sb += a.part[(int64_t)b * 2 * a.H + a.H + c];
+// dgamma[c] (+)= sum_b part[b][c], dbeta[c] (+)= sum_b part[b][H + c].  A
+// workgroup covers 32 columns of the 2H partial row with 8 row groups: group
+// t sums the blocks b = t, t + 8, ... in order, then the eight group sums
+// are added in group order (a fixed order: the result is deterministic).
+constexpr int kRedCols = 32, kRedGroups = 8;
+__global__ __launch_bounds__(kRedCols * kRedGroups) void ln_reduce_kernel(LnArgs a) {
+  __shared__ float red[kRedGroups][kRedCols];
+  const int lc = threadIdx.x % kRedCols, t = threadIdx.x / kRedCols;
+  const int c = blockIdx.x * kRedCols + lc;  // column of the [2H] partial row
+  const int W = 2 * a.H;
+  float s = 0.f;
+  if (c < W) {
+    for (int b = t; b < a.nblocks; b += kRedGroups) s += a.part[(int64_t)b * W + c];
   }
-  if (a.accumulate) {
-    a.dgamma[c] += sg;
-    a.dbeta[c] += sb;
-  } else {
-    a.dgamma[c] = sg;
-    a.dbeta[c] = sb;
+  red[t][lc] = s;
+  __syncthreads();
+  if (t == 0 && c < W) {
+    float tot = red[0][lc];
+#pragma unroll
+    for (int u = 1; u < kRedGroups; ++u) tot += red[u][lc];
+    float* dst = c < a.H ? a.dgamma + c : a.dbeta + (c - a.H);
+    if (a.accumulate) *dst += tot;
+    else *dst = tot;
   }
 }
 
@@ -229,10 +273,17 @@ hipError_t launch_ln_bwd(const LnArgs& a, hipStream_t stream) {
     return hipErrorInvalidValue;
   LnArgs b = a;
   b.nblocks = (int)((a.rows + a.rows_per_block - 1) / a.rows_per_block);
-  hipLaunchKernelGGL(ln_bwd_kernel, dim3((unsigned)b.nblocks), dim3(kLnThreads), 0, stream, b);
+  const dim3 grid((unsigned)b.nblocks), block(kLnThreads);
+  switch ((a.H + 2047) / 2048) {
+    case 1: hipLaunchKernelGGL(ln_bwd_kernel<1>, grid, block, 0, stream, b); break;
+    case 2: hipLaunchKernelGGL(ln_bwd_kernel<2>, grid, block, 0, stream, b); break;
+    case 3: hipLaunchKernelGGL(ln_bwd_kernel<3>, grid, block, 0, stream, b); break;
+    default: hipLaunchKernelGGL(ln_bwd_kernel<4>, grid, block, 0, stream, b); break;
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(ln_reduce_kernel, dim3((unsigned)((a.H + 255) / 256)), dim3(256), 0, stream, b);
+  hipLaunchKernelGGL(ln_reduce_kernel, dim3((unsigned)((2 * a.H + kRedCols - 1) / kRedCols)),
+                     dim3(kRedCols * kRedGroups), 0, stream, b);
   return hipGetLastError();
 }
 

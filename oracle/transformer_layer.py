@@ -33,7 +33,7 @@ Pins (tests/test_oracle_layer_pins.py): central finite differences of L for
 every input and parameter; the LayerNorm's moments; gelu's identities
 gelu(x) - gelu(-x) = x, gelu'(0) = 1/2 and its finite difference; the closed
 form Wo = W2 = 0 (then y = x and dx = dy); the walk equals the unchunked
-layer.
+layer; y at sampled rows from a prefix equals those rows of the full forward.
 """
 from __future__ import annotations
 
@@ -137,6 +137,35 @@ def layer_backward(x, dy, p, f, hq, hkv, d):
     # u = LN1(x); x also feeds h directly
     dx_ln, dg1, db1 = layer_norm_bwd(x, p["g1"], f["m1"], f["r1"], du)
     return dict(dx=dh + dx_ln, dw_qkv=dw_qkv, dw_o=dw_o, dw_1=dw_1, dw_2=dw_2, dg1=dg1, db1=db1, dg2=dg2, db2=db2)
+
+
+def layer_forward_rows(x, p, rows, hq, hkv, d, scale=None):
+    """y at the given rows only, from the prefix x [R, H] (R > max(rows)):
+    the causal layer's row r depends on rows 0..r alone, so this needs the
+    K/V projections of the prefix and, per sampled row, its own query, one
+    softmax per head over its visible keys, and the row-wise rest of the
+    block.  Returns [len(rows), H]."""
+    x = _f64(x)
+    H = x.shape[1]
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    G = hq // hkv
+    w = _f64(p["w_qkv"])
+    u, _, _ = layer_norm(x, p["g1"], p["b1"])
+    k = u @ w[:, hq * d:(hq + hkv) * d]
+    v = u @ w[:, (hq + hkv) * d:]
+    out = np.empty((len(rows), H))
+    for i, r in enumerate(rows):
+        q = u[r] @ w[:, :hq * d]
+        o = np.empty(hq * d)
+        for h in range(hq):
+            kv = slice((h // G) * d, (h // G + 1) * d)
+            s = (k[:r + 1, kv] @ q[h * d:(h + 1) * d]) * scale
+            e = np.exp(s - s.max())
+            o[h * d:(h + 1) * d] = (e / e.sum()) @ v[:r + 1, kv]
+        hr = x[r] + o @ _f64(p["w_o"])
+        z, _, _ = layer_norm(hr[None, :], p["g2"], p["b2"])
+        out[i] = hr + gelu(z[0] @ _f64(p["w_1"])) @ _f64(p["w_2"])
+    return out
 
 
 def layer(x, dy, p, hq, hkv, d, scale=None):

@@ -175,3 +175,20 @@ def test_layer_matches_torch_autograd(hq, hkv):
         np.testing.assert_allclose(got["d" + name], tp[name].grad.numpy(), rtol=1e-10, atol=1e-11, err_msg=name)
     for name, key in (("g1", "dg1"), ("b1", "db1"), ("g2", "dg2"), ("b2", "db2")):
         np.testing.assert_allclose(got[key], tp[name].grad.numpy(), rtol=1e-10, atol=1e-11, err_msg=name)
+
+
+@pytest.mark.parametrize("hq,hkv", [(2, 1), (4, 2)])
+def test_sampled_rows_equal_the_full_forward(hq, hkv):
+    # y at chosen rows, from a longer prefix, equals those rows of the full
+    # forward (causality: later rows of the prefix do not matter).
+    rng = np.random.default_rng(7)
+    d, S = 4, 13
+    h = hq * d
+    p = params(rng, h=h, hq=hq, hkv=hkv, d=d)
+    x = rng.normal(size=(S, h))
+    full = T.layer_forward(x, p, hq, hkv, d)["y"]
+    rows = [0, 1, 5, 11]
+    got = T.layer_forward_rows(x, p, rows, hq, hkv, d)
+    np.testing.assert_allclose(got, full[rows], rtol=1e-12, atol=1e-12)
+    got_short = T.layer_forward_rows(x[:12], p, rows, hq, hkv, d)
+    np.testing.assert_allclose(got_short, full[rows], rtol=1e-12, atol=1e-12)

@@ -34,7 +34,9 @@ Reported (one JSON line):
                  steps (kept out of the headline steps)
   --sweep-n      replaces all of the above by one line per chunk count
   cpu_baseline   the fp64 oracle on a bounded sample (two heads, a prefix of
-                 the sequence), in algorithmic TFLOP/s
+                 the sequence), in algorithmic TFLOP/s, with the CPU model and
+                 extrapolated_full_step_s: the whole step's algorithmic flop at
+                 that rate (an extrapolation, not a measurement)
 """
 from __future__ import annotations
 
@@ -74,6 +76,17 @@ def algorithmic_flops(offsets, B, Hq, D):
     (dQ; its S/dP recomputation is not credited) per visible pair and head."""
     p = sum(pairs_per_chunk(offsets)) * B * Hq * D
     return {"fwd": 4 * p, "bwd_dkdv": 8 * p, "bwd_dq": 2 * p, "bwd_pre": 0, "total": 14 * p}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def oracle_cpu_baseline(inp, D, sample_tokens, sample_heads):
@@ -323,6 +336,9 @@ def layer_bench(args):
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU layer oracle sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = layer_cpu_baseline(inp, p, Hq, Hkv, D, args.layer_cpu_tokens)
+        res["cpu_baseline"]["cpu_model"] = cpu_model()
+        # an extrapolation from the measured rate, not a measurement
+        res["cpu_baseline"]["extrapolated_full_step_s"] = total / (res["cpu_baseline"]["value"] * 1e12)
     print(json.dumps(res), flush=True)
 
 
@@ -574,6 +590,9 @@ def main():
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         cb = oracle_cpu_baseline(inp, D, args.cpu_sample_tokens, args.cpu_sample_heads)
         res["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+        res["cpu_baseline"]["cpu_model"] = cpu_model()
+        # an extrapolation from the measured rate, not a measurement
+        res["cpu_baseline"]["extrapolated_full_step_s"] = flops["total"] / (cb["value"] * 1e12)
     print(json.dumps(res), flush=True)
 
 

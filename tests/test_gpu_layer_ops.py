@@ -51,7 +51,8 @@ def test_layernorm_fwd_bwd(rows, H, ld):
     torch.cuda.synchronize()
     xh, dyh, dresh = to_np(x)[:, :H], to_np(dy)[:, :H], to_np(dres)[:, :H]
     ref_y, ref_m, ref_r = T.layer_norm(xh, to_np(gamma), to_np(beta))
-    got_y = to_np(y)[:, :H]
+    assert torch.isnan(y[:, H:]).all(), "columns past H written"
+    got_y = to_np(y[:, :H])
     assert np.abs(got_y - ref_y).max() <= 8e-3 * np.abs(ref_y).max()
     np.testing.assert_allclose(to_np(mean), ref_m, rtol=1e-5, atol=1e-5)
     np.testing.assert_allclose(to_np(rstd), ref_r, rtol=1e-4)

@@ -398,22 +398,57 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no LDS-DMA in flight past the stream
   }
 
-  // Write back rows [k0, k0+128) n [kv0, kv1): lane <-> d, v <-> key.
+  // Write back rows [k0, k0+128) n [kv0, kv1): lane <-> d, v <-> key.  In
+  // accumulate mode the 32 old values of a d-block are loaded before any of
+  // them is stored (dK and dV are distinct buffers, which the C ABI checks),
+  // so the loads share one memory round trip instead of one each (the sum
+  // is old + dK * scale in one fused multiply-add).  A block
+  // whose 128 keys are all in range (every one but a ragged last) takes a
+  // branch-free path: key v of the lane sits a compile-time number of rows
+  // past the lane's first key.
+  float* __restrict__ gdk = a.dk;
+  float* __restrict__ gdv = a.dv;
+  const int64_t rs = (int64_t)a.Hkv * D;  // elements between consecutive keys
+  const int64_t key0 = k0 + 32 * w + 4 * g;
+  const int64_t base = ((b * a.S + key0) * a.Hkv + hk) * D + l32;
+  auto koff = [](int v) { return 8 * (v / 4) + (v % 4); };
+  if (k0 + 128 <= kv1) {
 #pragma unroll
-  for (int db = 0; db < ND; ++db) {
+    for (int db = 0; db < ND; ++db) {
+      float* pk = gdk + base + 32 * db;
+      float* pv = gdv + base + 32 * db;
+      float ok[16], ov[16];
+      if (a.accumulate) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int64_t key = k0 + 32 * w + 8 * (v / 4) + 4 * g + (v % 4);
-      if (key < kv1) {
-        const int64_t idx = ((b * a.S + key) * a.Hkv + hk) * D + 32 * db + l32;
-        const float kval = dk[db][v] * a.scale;
-        const float vval = dv[db][v];
-        if (a.accumulate) {
-          a.dk[idx] += kval;
-          a.dv[idx] += vval;
-        } else {
-          a.dk[idx] = kval;
-          a.dv[idx] = vval;
+        for (int v = 0; v < 16; ++v) {
+          ok[v] = pk[koff(v) * rs];
+          ov[v] = pv[koff(v) * rs];
+        }
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        pk[koff(v) * rs] = a.accumulate ? __builtin_fmaf(dk[db][v], a.scale, ok[v]) : dk[db][v] * a.scale;
+        pv[koff(v) * rs] = a.accumulate ? ov[v] + dv[db][v] : dv[db][v];
+      }
+    }
+  } else {
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+      float ok[16], ov[16];
+      if (a.accumulate) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int64_t idx = base + koff(v) * rs + 32 * db;
+          ok[v] = key0 + koff(v) < kv1 ? gdk[idx] : 0.f;
+          ov[v] = key0 + koff(v) < kv1 ? gdv[idx] : 0.f;
+        }
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        if (key0 + koff(v) < kv1) {
+          const int64_t idx = base + koff(v) * rs + 32 * db;
+          gdk[idx] = a.accumulate ? __builtin_fmaf(dk[db][v], a.scale, ok[v]) : dk[db][v] * a.scale;
+          gdv[idx] = a.accumulate ? ov[v] + dv[db][v] : dv[db][v];
         }
       }
     }

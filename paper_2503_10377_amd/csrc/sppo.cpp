@@ -514,6 +514,7 @@ sppo_status sppo_attn_bwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i, const
       (st = check_ptr(ctx, dk_acc, "dk_acc")) || (st = check_ptr(ctx, dv_acc, "dv_acc"))) {
     return st;
   }
+  if (dk_acc == dv_acc) return fail(ctx, SPPO_ERR_INVALID_ARG, "dk_acc and dv_acc must be distinct buffers");
   if (!ctx->in_bwd || i != ctx->next_bwd) {
     return fail(ctx, SPPO_ERR_ORDER, "backward of chunk " + std::to_string(i) + " out of order (expected " +
                                          (ctx->in_bwd ? std::to_string(ctx->next_bwd) : std::string("the forward pass to finish")) + ")");

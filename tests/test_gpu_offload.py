@@ -246,6 +246,9 @@ def test_order_and_state_errors():
     assert status_of(L.sppo_attn_fwd_chunk, ctx, 1, qc[1], k, v, oc[1], lse[1]) == L.SPPO_ERR_ORDER
     assert status_of(L.sppo_attn_bwd_chunk, ctx, 3, qc[3], k, v, oc[3], lse[3], dc[3], dqc[3],
                      out["dk"], out["dv"]) == L.SPPO_ERR_ORDER
+    # dK and dV must be distinct accumulators (checked before the order)
+    assert status_of(L.sppo_attn_bwd_chunk, ctx, 3, qc[3], k, v, oc[3], lse[3], dc[3], dqc[3],
+                     out["dk"], out["dk"]) == L.SPPO_ERR_INVALID_ARG
     assert status_of(L.sppo_offload_issue, ctx, 0, bufs(0)) == L.SPPO_ERR_STATE  # before its fwd
     assert status_of(L.sppo_prefetch, ctx, 0, bufs(0)) == L.SPPO_ERR_STATE       # never offloaded
     assert status_of(L.sppo_offload_wait, ctx, 0) == L.SPPO_ERR_STATE

@@ -170,7 +170,13 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_kernel(GemmArgs g) {
     compute(A0, B0);
   }
 
-  // ---- epilogue: lane <-> column n, v <-> row m; one 32 x 32 tile at a time
+  // ---- epilogue: lane <-> column n, v <-> row m; one 32 x 32 tile at a time.
+  // Epilogues that read (the residual, the GELU pre-activation, the fp32
+  // accumulator) load the tile's 16 values of the lane before storing any
+  // result, so the loads share one memory round trip instead of one each; a
+  // tile whose 32 rows are all below M takes a branch-free path.
+  constexpr bool kLoads = EPI == kEpiAddBf16 || EPI == kEpiDGelu || EPI == kEpiAccF32;
+  auto roff = [](int v) { return 8 * (v / 4) + (v % 4); };
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
@@ -178,31 +184,51 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_kernel(GemmArgs g) {
       __builtin_amdgcn_sched_barrier(0);
       const int64_t n = n0 + wn * 128 + 32 * nt + l32;
       const int64_t mb = m0 + wm * 64 + 32 * mt + 4 * gh;
+      const bool full = m0 + wm * 64 + 32 * mt + 32 <= g.M;  // uniform over the wave
+      // element offsets from C / aux fit 32 bits (checked by the C ABI): one
+      // register per address, on the wave-uniform base pointer
+      const uint32_t cb = (uint32_t)(mb * g.ldc + n), ab = (uint32_t)(mb * g.ldaux + n);
+      const uint32_t cs = (uint32_t)g.ldc, as = (uint32_t)g.ldaux;
       if (n < g.N) {
+        // in halves of eight rows: the eight loads, then the eight results
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int64_t m = mb + 8 * (v / 4) + (v % 4);
-          if (m < g.M) {
-            const float x = acc[mt][nt][v];
-            const int64_t ic = m * g.ldc + n;
-            if constexpr (EPI == kEpiBf16) {
-              static_cast<__bf16*>(g.c)[ic] = (__bf16)x;
-            } else if constexpr (EPI == kEpiAddBf16) {
-              const float r = (float)reinterpret_cast<const __bf16*>(g.aux)[m * g.ldaux + n];
-              static_cast<__bf16*>(g.c)[ic] = (__bf16)(x + r);
-            } else if constexpr (EPI == kEpiGelu) {
-              const __bf16 pre = (__bf16)x;
-              reinterpret_cast<__bf16*>(g.aux)[m * g.ldaux + n] = pre;
-              static_cast<__bf16*>(g.c)[ic] = (__bf16)gelu_tanh((float)pre);
-            } else if constexpr (EPI == kEpiDGelu) {
-              const float pre = (float)reinterpret_cast<const __bf16*>(g.aux)[m * g.ldaux + n];
-              static_cast<__bf16*>(g.c)[ic] = (__bf16)(x * gelu_tanh_grad(pre));
-            } else if constexpr (EPI == kEpiAccF32) {
-              static_cast<float*>(g.c)[ic] += x;
-            } else {
-              static_cast<float*>(g.c)[ic] = x;
+        for (int hb = 0; hb < 2; ++hb) {
+          float in[8];
+          if constexpr (kLoads) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const int v = 8 * hb + u;
+              in[u] = 0.f;
+              if (full || mb + roff(v) < g.M) {
+                if constexpr (EPI == kEpiAccF32) in[u] = static_cast<const float*>(g.c)[cb + roff(v) * cs];
+                else in[u] = (float)reinterpret_cast<const __bf16*>(g.aux)[ab + roff(v) * as];
+              }
             }
           }
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const int v = 8 * hb + u;
+            if (full || mb + roff(v) < g.M) {
+              const float x = acc[mt][nt][v];
+              const uint32_t ic = cb + roff(v) * cs;
+              if constexpr (EPI == kEpiBf16) {
+                static_cast<__bf16*>(g.c)[ic] = (__bf16)x;
+              } else if constexpr (EPI == kEpiAddBf16) {
+                static_cast<__bf16*>(g.c)[ic] = (__bf16)(x + in[u]);
+              } else if constexpr (EPI == kEpiGelu) {
+                const __bf16 pre = (__bf16)x;
+                reinterpret_cast<__bf16*>(g.aux)[ab + roff(v) * as] = pre;
+                static_cast<__bf16*>(g.c)[ic] = (__bf16)gelu_tanh((float)pre);
+              } else if constexpr (EPI == kEpiDGelu) {
+                static_cast<__bf16*>(g.c)[ic] = (__bf16)(x * gelu_tanh_grad(in[u]));
+              } else if constexpr (EPI == kEpiAccF32) {
+                static_cast<float*>(g.c)[ic] = in[u] + x;
+              } else {
+                static_cast<float*>(g.c)[ic] = x;
+              }
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
     }

@@ -37,6 +37,8 @@ sppo_status sppo_gemm_bf16(int32_t layout, int64_t M, int64_t N, int64_t K, cons
   } else {
     return SPPO_ERR_INVALID_ARG;
   }
+  // the epilogue addresses C and aux by 32-bit element offsets
+  if (M * ldc >= ((int64_t)1 << 31) || (aux && M * ldaux >= ((int64_t)1 << 31))) return SPPO_ERR_UNSUPPORTED;
   // the DMA byte ranges of one tile fit 32 bits
   if ((layout == SPPO_GEMM_NT ? 256 : 64) * (lda > ldb ? lda : ldb) * 2 > INT32_MAX) return SPPO_ERR_UNSUPPORTED;
   sppo::GemmArgs g{};

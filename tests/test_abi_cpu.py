@@ -88,6 +88,10 @@ def test_layer_ops_reject_invalid_arguments_before_launch():
     assert lib.sppo_gemm_bf16(0, 128, 256, 64, a + 2, 64, a, 64, a, 256, 0, None, 0, None) == bad
     assert lib.sppo_gemm_bf16(0, 128, 256, 64, a, 64, a, 64, a, 256, 1, None, 0, None) == bad  # ADD needs aux
     assert lib.sppo_gemm_bf16(0, 0, 256, 64, a, 64, a, 64, a, 256, 0, None, 0, None) == bad
+    # the epilogue's 32-bit element offsets: M * ldc (and M * ldaux) below 2^31
+    unsup = 2  # SPPO_ERR_UNSUPPORTED
+    assert lib.sppo_gemm_bf16(0, 1 << 20, 4096, 64, a, 64, a, 64, a, 4096, 0, None, 0, None) == unsup
+    assert lib.sppo_gemm_bf16(0, 1 << 19, 256, 64, a, 64, a, 64, a, 256, 1, a, 8192, None) == unsup
     # LayerNorm: H % 8, H > 8192, eps <= 0
     assert lib.sppo_layernorm_fwd(4, 100, a, 100, a, a, 1e-5, a, 100, a, a, None) == bad
     assert lib.sppo_layernorm_fwd(4, 8200, a, 8200, a, a, 1e-5, a, 8200, a, a, None) == bad

@@ -332,9 +332,11 @@ const char* sppo_status_string(sppo_status s);
  *   DGELU     C = acc * gelu'(aux) (bf16)
  *   ACC_F32   C += acc (fp32): gradients accumulated over chunks
  *   F32       C = acc (fp32)
- * M * ldc and M * ldaux must stay below 2^31 elements (the epilogue
- * addresses C and aux by 32-bit element offsets): SPPO_ERR_UNSUPPORTED
- * otherwise. */
+ * N, ldc and ldaux must be multiples of 4 and aux 8-byte aligned (the
+ * epilogues use 8- and 16-byte vector accesses): SPPO_ERR_INVALID_ARG
+ * otherwise.  M * ldc and M * ldaux must stay below 2^31 elements (the
+ * epilogue addresses C and aux by 32-bit element offsets):
+ * SPPO_ERR_UNSUPPORTED otherwise. */
 typedef enum { SPPO_GEMM_NT = 0, SPPO_GEMM_TN = 1 } sppo_gemm_layout;
 typedef enum {
   SPPO_EPI_BF16 = 0,

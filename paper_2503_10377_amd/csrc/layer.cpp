@@ -25,10 +25,10 @@ sppo_status sppo_gemm_bf16(int32_t layout, int64_t M, int64_t N, int64_t K, cons
                            int64_t ldaux, void* stream) {
   if (M <= 0 || N <= 0 || K <= 0) return SPPO_ERR_INVALID_ARG;
   if (!al16(a) || !al16(b) || !al16(c)) return SPPO_ERR_INVALID_ARG;
-  if (lda % 8 || ldb % 8 || ldc <= 0) return SPPO_ERR_INVALID_ARG;
+  if (lda % 8 || ldb % 8 || ldc <= 0 || ldc % 4 || N % 4) return SPPO_ERR_INVALID_ARG;
   if (epilogue < SPPO_EPI_BF16 || epilogue > SPPO_EPI_F32) return SPPO_ERR_INVALID_ARG;
   const bool needs_aux = epilogue == SPPO_EPI_ADD_BF16 || epilogue == SPPO_EPI_GELU || epilogue == SPPO_EPI_DGELU;
-  if (needs_aux && (!aux || ldaux < N)) return SPPO_ERR_INVALID_ARG;
+  if (needs_aux && (!aux || ldaux < N || ldaux % 4 || (reinterpret_cast<uintptr_t>(aux) & 7))) return SPPO_ERR_INVALID_ARG;
   if (ldc < N) return SPPO_ERR_INVALID_ARG;
   if (layout == SPPO_GEMM_NT) {
     if (K % 64 || lda < K || ldb < K) return SPPO_ERR_INVALID_ARG;

@@ -88,6 +88,11 @@ def test_layer_ops_reject_invalid_arguments_before_launch():
     assert lib.sppo_gemm_bf16(0, 128, 256, 64, a + 2, 64, a, 64, a, 256, 0, None, 0, None) == bad
     assert lib.sppo_gemm_bf16(0, 128, 256, 64, a, 64, a, 64, a, 256, 1, None, 0, None) == bad  # ADD needs aux
     assert lib.sppo_gemm_bf16(0, 0, 256, 64, a, 64, a, 64, a, 256, 0, None, 0, None) == bad
+    # vector epilogues: N, ldc and ldaux multiples of 4, aux 8-byte aligned
+    assert lib.sppo_gemm_bf16(0, 128, 254, 64, a, 64, a, 64, a, 256, 0, None, 0, None) == bad
+    assert lib.sppo_gemm_bf16(0, 128, 256, 64, a, 64, a, 64, a, 258, 0, None, 0, None) == bad
+    assert lib.sppo_gemm_bf16(0, 128, 256, 64, a, 64, a, 64, a, 256, 1, a, 258, None) == bad
+    assert lib.sppo_gemm_bf16(0, 128, 256, 64, a, 64, a, 64, a, 256, 1, a + 4, 256, None) == bad
     # the epilogue's 32-bit element offsets: M * ldc (and M * ldaux) below 2^31
     unsup = 2  # SPPO_ERR_UNSUPPORTED
     assert lib.sppo_gemm_bf16(0, 1 << 20, 4096, 64, a, 64, a, 64, a, 4096, 0, None, 0, None) == unsup

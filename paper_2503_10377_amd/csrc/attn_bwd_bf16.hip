@@ -3,8 +3,9 @@
 // of SPPO) calls this for i = N-1..0; dK/dV accumulate across calls in fp32.
 //
 // Three kernels, all on the caller's stream:
-//   bwd_pre   Delta_r = <dO_r, O_r> and LSE2_r = LSE_r * log2(e) into the
-//             context's workspace (HBM-bound)
+//   bwd_pre   -Delta_r = -<dO_r, O_r> and LSE2_r = LSE_r * log2(e) into the
+//             context's workspace (HBM-bound); -Delta is the initial value
+//             of the dP accumulators, so the MFMAs produce dP - Delta
 //   bwd_dkdv  one workgroup per 128 keys of one KV head (4 waves x 32 keys,
 //             lane <-> key, K/V fragments in registers); the chunk's query
 //             rows of every head of the GQA group stream through LDS in
@@ -32,8 +33,9 @@ constexpr int kDqRows = 128;  // query rows per dQ workgroup (4 waves x 32)
 constexpr int kSB = 32;       // rows (dK/dV) or keys (dQ) per sub-block
 constexpr int kRing = 6;      // LDS ring slots
 constexpr int kAhead = 5;     // sub-blocks loaded ahead of the one in use
-// LSE2/Delta groups loaded ahead of their use in the softmax (0: right
-// before; 1: 1.3% faster at 128K; all four at the step start: 0.9%).
+// LSE2 groups loaded ahead of their use in the softmax (0: right before;
+// 1: 1.3% faster at 128K, measured when the Delta groups went with them;
+// all four at the step start: 0.9%).
 constexpr int kLdAhead = 1;
 // The B phase's first three transposed reads are issued in the last MFMA
 // slots of the A phase, which read nothing else (dQ 1% faster than issuing
@@ -71,7 +73,7 @@ __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(ChunkArgs a) {
     const int64_t rr = (item / a.Hq) % s;
     const int64_t b = item / (a.Hq * s);
     const int64_t idx = (b * a.Hq + h) * s + rr;
-    a.delta[idx] = acc;
+    a.delta[idx] = -acc;
     a.lse2[idx] = a.lse[idx] * kLog2e;
   }
 }
@@ -83,8 +85,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   constexpr int P = T::P, NK = D / 16, ND = D / 32;
   constexpr int IPWQ = (kSB / T::RPI) / 4;  // DMA instructions per wave per tensor per sub-block
   static_assert(IPWQ >= 1 && IPWQ * 4 * T::RPI == kSB, "sub-block splits over 4 waves");
-  constexpr int DMA_PER_SB = 2 * IPWQ + 1;  // Q, dO, and one for the [LSE2 | Delta] record
-  // One LDS object per ring slot: [Q rows | dO rows | LSE2 (32 floats) | Delta (32 floats)].
+  constexpr int DMA_PER_SB = 2 * IPWQ + 1;  // Q, dO, and one for the [LSE2 | -Delta] record
+  // One LDS object per ring slot: [Q rows | dO rows | LSE2 (32 floats) | -Delta (32 floats)].
   constexpr int SLOT = 2 * kSB * P + 128;
   __shared__ __attribute__((aligned(1024))) uint16_t R0[SLOT], R1[SLOT], R2[SLOT], R3[SLOT], R4[SLOT], R5[SLOT];
   auto slot = [&](auto I) -> uint16_t* {
@@ -129,8 +131,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   int dmaq[IPWQ];
 #pragma unroll
   for (int x = 0; x < IPWQ; ++x) dmaq[x] = T::dma(lane, w * IPWQ + x, qstride);
-  // The [LSE2 | Delta] record: waves 0, 1 load LSE2 rows 0..15, 16..31, waves
-  // 2, 3 Delta, 16 lanes each.
+  // The [LSE2 | -Delta] record: waves 0, 1 load LSE2 rows 0..15, 16..31,
+  // waves 2, 3 -Delta, 16 lanes each.
   const int dmal = (16 * (w & 1) + (lane & 15)) * 4;
   const float* lsrc = (w < 2) ? a.lse2 : a.delta;
   const int ldst = 32 * (w >> 1) + 16 * (w & 1);
@@ -206,10 +208,25 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   auto tr_rd = [&](const uint16_t* X, int hh, int db) {
     return ld_tr(X, tro[db][0] + 16 * hh * P, tro[db][1] + 16 * hh * P);
   };
-  // S = Q K^T and dP = dO V^T of one sub-block (lane <-> key).
+  // -Delta of the 16 rows 8 (v/4) + 4 g + v%4 of a sub-block, from its record:
+  // the initial value of its dP accumulator.
+  auto ndelta = [&](const float* ld) {
+    f32x16 x;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float4 t = *reinterpret_cast<const float4*>(ld + 32 + 8 * k + 4 * g);
+      x[4 * k] = t.x;
+      x[4 * k + 1] = t.y;
+      x[4 * k + 2] = t.z;
+      x[4 * k + 3] = t.w;
+    }
+    return x;
+  };
+  // S = Q K^T and dP - Delta = dO V^T - Delta of one sub-block (lane <-> key);
+  // dp holds -Delta on entry.
   auto sdp = [&](const uint16_t* Qs, const uint16_t* Os, f32x16& sv, f32x16& dp) {
     sv = mfma32(ld_nat(Qs, nat[0]), kf[0], f32x16{});
-    dp = mfma32(ld_nat(Os, nat[0]), vf[0], f32x16{});
+    dp = mfma32(ld_nat(Os, nat[0]), vf[0], dp);
 #pragma unroll
     for (int kk = 1; kk < NK; ++kk) {
       sv = mfma32(ld_nat(Qs, nat[kk]), kf[kk], sv);
@@ -240,9 +257,9 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
       issue(h, sb, qbuf(IC<0>{}), obuf(IC<0>{}), lbuf(IC<0>{}));
       __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
       __syncthreads();
-      f32x16 sv, dp;
-      sdp(qbuf(IC<0>{}), obuf(IC<0>{}), sv, dp);
       const float* ld = lbuf(IC<0>{});
+      f32x16 sv, dp = ndelta(ld);
+      sdp(qbuf(IC<0>{}), obuf(IC<0>{}), sv, dp);
       const int64_t r0g = c0 + (int64_t)sb * kSB;  // global row of the sub-block's first row
       float p[16], ds[16];
 #pragma unroll
@@ -251,7 +268,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
         float pv = fast_exp2(sv[v] * C - ld[qi]);
         if (j > r0g + qi) pv = 0.f;  // key j sees row r iff j <= r
         p[v] = pv;
-        ds[v] = pv * (dp[v] - ld[32 + qi]);
+        ds[v] = pv * dp[v];
       }
       bf16x8 pb[2], dsb[2];
       pb[0] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
@@ -275,18 +292,21 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
     // end of the previous B phase.
     __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - (kEarlyA ? 2 : 1)) * DMA_PER_SB));
     __syncthreads();
-    f32x16 sa, da, sb2, db2;
+    f32x16 sa, da = ndelta(lbuf(IC<0>{})), sb2, db2;
     sdp(qbuf(IC<0>{}), obuf(IC<0>{}), sa, da);
     bf16x8 opn[4];
     if (kEarlyA) {
 #pragma unroll
       for (int m = 0; m < 4; ++m) opn[m] = ld_nat((m & 1) ? obuf(IC<1>{}) : qbuf(IC<1>{}), nat[m >> 1]);
+      db2 = ndelta(lbuf(IC<1>{}));
     }
     // Step n in slot I: A(n) reads slot I+1 (natural) and slot I's record;
     // B(n) reads slot I (transposed) and, in its last MFMA slots, A(n+1)'s
     // first natural operands from slot I+2.  At its start sub-blocks n+1 and
     // n+2 have landed (only n+3, n+4 may still be loading); then sub-block
-    // n+5 goes to slot I+5 = I-1, free since step n-1.
+    // n+5 goes to slot I+5 = I-1, free since step n-1.  dnext holds -Delta of
+    // sub-block n+1 on entry (read in B(n-1)); B(n) leaves -Delta of n+2 in
+    // dcur, which is step n+1's dnext.
     auto step = [&](int n, auto sl, f32x16& scur, f32x16& dcur, f32x16& snext, f32x16& dnext) {
       constexpr int I = decltype(sl)::value;
       constexpr int I1 = (I + 1) % kRing, I2 = (I + 2) % kRing, I5 = (I + kAhead) % kRing;
@@ -298,6 +318,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
       const uint16_t* Qc = qbuf(IC<I>{});
       const uint16_t* Oc = obuf(IC<I>{});
       const float* ld = lbuf(IC<I>{});
+      if (!kEarlyA) dnext = ndelta(lbuf(IC<I1>{}));
       // A(n): MFMA m (NA of them) is S(n+1) (m even) or dP(n+1) (m odd),
       // k-step m/2; its operand is read four MFMAs ahead.  The VALU turns the
       // 16 elements of S(n), dP(n) into P(n), dS(n), element i beside MFMA
@@ -307,13 +328,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
       bf16x8 op[NA];
 #pragma unroll
       for (int m = 0; m < 4; ++m) op[m] = kEarlyA ? opn[m] : nat_op(m);
-      // LSE2 and Delta of rows 8 k + 4 g .. + 3 (group k of four elements),
-      // loaded kLdAhead groups before their use.
-      float4 lgk[4], dgk[4];
-      auto ld_group = [&](int k) {
-        lgk[k] = *reinterpret_cast<const float4*>(ld + 8 * k + 4 * g);
-        dgk[k] = *reinterpret_cast<const float4*>(ld + 32 + 8 * k + 4 * g);
-      };
+      // LSE2 of rows 8 k + 4 g .. + 3 (group k of four elements), loaded
+      // kLdAhead groups before its use.
+      float4 lgk[4];
+      auto ld_group = [&](int k) { lgk[k] = *reinterpret_cast<const float4*>(ld + 8 * k + 4 * g); };
 #pragma unroll
       for (int k = 0; k <= kLdAhead && k < 4; ++k) ld_group(k);
       float p[16], ds[16];
@@ -333,7 +351,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
         if (i % EPM == 0) {
           const int mi = i / EPM;
           if (mi & 1) {
-            dnext = mfma32(op[mi], vf[mi >> 1], mi == 1 ? f32x16{} : dnext);
+            dnext = mfma32(op[mi], vf[mi >> 1], dnext);
           } else {
             snext = mfma32(op[mi], kf[mi >> 1], mi == 0 ? f32x16{} : snext);
           }
@@ -341,11 +359,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
           else if (kEarlyTr && mi + 4 - NA < 3) top[mi + 4 - NA] = tr_op(mi + 4 - NA);
         }
         const int e = i & 3;
-        const float4 l4 = lgk[i >> 2], d4 = dgk[i >> 2];
+        const float4 l4 = lgk[i >> 2];
         const float lv = e == 0 ? l4.x : e == 1 ? l4.y : e == 2 ? l4.z : l4.w;
-        const float dl = e == 0 ? d4.x : e == 1 ? d4.y : e == 2 ? d4.z : d4.w;
         p[i] = fast_exp2(scur[i] * C - lv);
-        ds[i] = p[i] * (dcur[i] - dl);
+        ds[i] = p[i] * dcur[i];
         if (e == 3 && i < 15) {  // rows 8 (v/4) + 4 g + v%4 of the next group of four
           if ((i >> 2) + kLdAhead + 1 < 4) ld_group((i >> 2) + kLdAhead + 1);
         }
@@ -372,10 +389,13 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
         }
         if (jj + 3 < NB) {
           top[jj + 3] = tr_op(jj + 3);
-        } else if (kEarlyA) {  // A(n+1)'s first natural operands, from sub-block n+2
+        } else if (kEarlyA) {  // A(n+1)'s first natural operands and -Delta, from sub-block n+2
           const int m0 = jj + 3 - NB;
           opn[m0] = ld_nat((m0 & 1) ? obuf(IC<I2>{}) : qbuf(IC<I2>{}), nat[m0 >> 1]);
-          if (m0 == 2) opn[3] = ld_nat(obuf(IC<I2>{}), nat[1]);
+          if (m0 == 2) {
+            opn[3] = ld_nat(obuf(IC<I2>{}), nat[1]);
+            dcur = ndelta(lbuf(IC<I2>{}));
+          }
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -507,7 +527,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
   const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + (b * a.S * a.Hkv + hk) * D;
 
   bf16x8 qf[NK], df[NK];
-  float lse2 = INFINITY, dl = 0.f;  // a padding row gets P = 0
+  float lse2 = INFINITY, ndl = 0.f;  // a padding row gets P = 0
   if (rvalid) {
     const int64_t off = ((b * s + (r - c0)) * a.Hq + h) * D;
     const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + off;
@@ -518,7 +538,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
       df[kk] = as_bf16x8(ld_global16(drow + 16 * kk + 8 * g));
     }
     lse2 = a.lse2[(b * a.Hq + h) * s + (r - c0)];
-    dl = a.delta[(b * a.Hq + h) * s + (r - c0)];
+    ndl = a.delta[(b * a.Hq + h) * s + (r - c0)];
   } else {
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) qf[kk] = df[kk] = bf16x8{};
@@ -526,6 +546,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
   f32x16 dq[ND];
 #pragma unroll
   for (int db = 0; db < ND; ++db) dq[db] = f32x16{};
+  // -Delta of the lane's row in every element: the initial value of each dP^T
+  // accumulator, so the MFMAs produce dP^T - Delta.
+  f32x16 ninit;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) ninit[v] = ndl;
 
   // DMA of K/V sub-block u (keys [32u, 32u+32)) into a slot; keys past the
   // chunk end load zeros, so every call issues DMA_PER_SB instructions.
@@ -551,11 +576,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
   auto tr_rd = [&](const uint16_t* X, int hh, int db) {
     return ld_tr(X, tro[db][0] + 16 * hh * P, tro[db][1] + 16 * hh * P);
   };
-  // S^T = K Q^T and dP^T = V dO^T of one sub-block (lane <-> query).
+  // S^T = K Q^T and dP^T - Delta = V dO^T - Delta of one sub-block (lane <-> query).
   auto sdp = [&](const uint16_t* K, f32x16& sv, f32x16& dp) {
     const uint16_t* V = K + kSB * P;
     sv = mfma32(ld_nat(K, nat[0]), qf[0], f32x16{});
-    dp = mfma32(ld_nat(V, nat[0]), df[0], f32x16{});
+    dp = mfma32(ld_nat(V, nat[0]), df[0], ninit);
 #pragma unroll
     for (int kk = 1; kk < NK; ++kk) {
       sv = mfma32(ld_nat(K, nat[kk]), qf[kk], sv);
@@ -617,7 +642,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
         if (i % EPM == 0) {
           const int mi = i / EPM;
           if (mi & 1) {
-            dnext = mfma32(op[mi], df[mi >> 1], mi == 1 ? f32x16{} : dnext);
+            dnext = mfma32(op[mi], df[mi >> 1], mi == 1 ? ninit : dnext);
           } else {
             snext = mfma32(op[mi], qf[mi >> 1], mi == 0 ? f32x16{} : snext);
           }
@@ -625,7 +650,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
           else if (kEarlyTr && mi + 4 - NA < 3) top[mi + 4 - NA] = tr_op(mi + 4 - NA);
         }
         const float p = fast_exp2(scur[i] * C - lse2);
-        ds[i] = p * (dcur[i] - dl);
+        ds[i] = p * dcur[i];
         if ((i & 7) == 7) {
           const int h8 = i >> 3, q = 8 * h8;
           dsb[h8] = pack_bf16x8(ds[q], ds[q + 1], ds[q + 2], ds[q + 3], ds[q + 4], ds[q + 5], ds[q + 6], ds[q + 7]);
@@ -681,7 +706,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
     for (int v = 0; v < 16; ++v) {
       float p = fast_exp2(sv[v] * C - lse2);
       if (8 * (v / 4) + 4 * g + (v % 4) > rel) p = 0.f;
-      ds[v] = p * (dp[v] - dl);
+      ds[v] = p * dp[v];
     }
     bf16x8 dsb[2];
     dsb[0] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);

@@ -19,7 +19,7 @@ struct ChunkArgs {
   void* dq;            // [B, s, Hq, D]
   float* dk;           // [B, S, Hkv, D] fp32 accumulator
   float* dv;           // [B, S, Hkv, D] fp32 accumulator
-  float* delta;        // [B, Hq, s]     workspace: <dO_r, O_r>
+  float* delta;        // [B, Hq, s]     workspace: <dO_r, O_r> (fp32 kernels) or its negation (bf16)
   float* lse2;         // [B, Hq, s]     workspace: LSE * log2(e) (bf16 backward)
   int64_t B, S, c0, c1;
   int Hq, Hkv, D;

@@ -361,18 +361,22 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
         const int e = i & 3;
         const float4 l4 = lgk[i >> 2];
         const float lv = e == 0 ? l4.x : e == 1 ? l4.y : e == 2 ? l4.z : l4.w;
+        // Element i's exp, element i-1's dS: an exp's result is not read by the
+        // next instruction (that would cost a wait state).
         p[i] = fast_exp2(scur[i] * C - lv);
-        ds[i] = p[i] * dcur[i];
+        if (i > 0) ds[i - 1] = p[i - 1] * dcur[i - 1];
         if (e == 3 && i < 15) {  // rows 8 (v/4) + 4 g + v%4 of the next group of four
           if ((i >> 2) + kLdAhead + 1 < 4) ld_group((i >> 2) + kLdAhead + 1);
         }
-        if ((i & 7) == 7) {
-          const int h8 = i >> 3, q = 8 * h8;
-          pb[h8] = pack_bf16x8(p[q], p[q + 1], p[q + 2], p[q + 3], p[q + 4], p[q + 5], p[q + 6], p[q + 7]);
-          dsb[h8] = pack_bf16x8(ds[q], ds[q + 1], ds[q + 2], ds[q + 3], ds[q + 4], ds[q + 5], ds[q + 6], ds[q + 7]);
+        if (i == 8) {
+          pb[0] = pack_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+          dsb[0] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
         }
         if (i % EPM == EPM - 1) __builtin_amdgcn_sched_barrier(0);
       }
+      ds[15] = p[15] * dcur[15];
+      pb[1] = pack_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
+      dsb[1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
       if (!kEarlyTr) {
         top[0] = tr_op(0);
         top[1] = tr_op(1);
@@ -628,7 +632,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
       bf16x8 op[NA];
 #pragma unroll
       for (int m = 0; m < 4; ++m) op[m] = kEarlyAq ? opn[m] : nat_op(m);
-      float ds[16];
+      float pv[16], ds[16];
       bf16x8 dsb[2];
       // B(n): MFMA jj is dQ^T d-block jj % ND for k-half jj / ND; its
       // transposed K operand is read three slots ahead (the first three in
@@ -649,14 +653,14 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
           if (mi + 4 < NA) op[mi + 4] = nat_op(mi + 4);
           else if (kEarlyTr && mi + 4 - NA < 3) top[mi + 4 - NA] = tr_op(mi + 4 - NA);
         }
-        const float p = fast_exp2(scur[i] * C - lse2);
-        ds[i] = p * dcur[i];
-        if ((i & 7) == 7) {
-          const int h8 = i >> 3, q = 8 * h8;
-          dsb[h8] = pack_bf16x8(ds[q], ds[q + 1], ds[q + 2], ds[q + 3], ds[q + 4], ds[q + 5], ds[q + 6], ds[q + 7]);
-        }
+        // Element i's exp, element i-1's dS (no exp result read right away).
+        pv[i] = fast_exp2(scur[i] * C - lse2);
+        if (i > 0) ds[i - 1] = pv[i - 1] * dcur[i - 1];
+        if (i == 8) dsb[0] = pack_bf16x8(ds[0], ds[1], ds[2], ds[3], ds[4], ds[5], ds[6], ds[7]);
         if (i % EPM == EPM - 1) __builtin_amdgcn_sched_barrier(0);
       }
+      ds[15] = pv[15] * dcur[15];
+      dsb[1] = pack_bf16x8(ds[8], ds[9], ds[10], ds[11], ds[12], ds[13], ds[14], ds[15]);
       if (!kEarlyTr) {
         top[0] = tr_op(0);
         top[1] = tr_op(1);

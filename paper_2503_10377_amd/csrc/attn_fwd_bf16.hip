@@ -188,7 +188,9 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
     for (int y = 0; y < 4; ++y) s4[y] = (p[4 * y] + p[4 * y + 1]) + (p[4 * y + 2] + p[4 * y + 3]);
     lsum += (s4[0] + s4[1]) + (s4[2] + s4[3]);
     const float mx = row_max(snext);
-    // A: four K reads up front, then per MFMA one more read and ~5 VALU ops.
+    // A: four K reads up front, then per MFMA one more read and ~5 VALU ops;
+    // no VALU right after the last S^T MFMA (what is left is the row max of
+    // S^T(u+1), which would wait for that MFMA to finish).
     SGB(kSgDSRead, 4);
     SGB(kSgVALU, 6);
 #pragma unroll
@@ -199,12 +201,15 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
       } else {
         SGB(kSgDSRead, 2);
       }
-      SGB(kSgVALU, 5);
+      if (i < NK - 1) SGB(kSgVALU, 5);
     }
-    // B: the remaining V reads, then the PV MFMAs with the sums and the max.
+    // B: the first PV MFMA, the remaining V reads, then the other PV MFMAs
+    // with the sums and the max.
+    SGB(kSgMFMA, 1);
     SGB(kSgDSRead, 8);
+    SGB(kSgVALU, 4);
 #pragma unroll
-    for (int i = 0; i < 2 * ND; ++i) {
+    for (int i = 1; i < 2 * ND; ++i) {
       SGB(kSgMFMA, 1);
       SGB(kSgVALU, 4);
     }

@@ -29,7 +29,7 @@ constexpr int kFwdBC = 64;       // keys per V tile (two K sub-blocks)
 constexpr float kLazyMax = 8.f;  // log2 headroom before the running max moves
 
 #define SGB(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
-constexpr int kSgMFMA = 0x008, kSgVALU = 0x002, kSgDSRead = 0x100;
+constexpr int kSgMFMA = 0x008, kSgVALU = 0x002, kSgDSRead = 0x100, kSgTrans = 0x400;
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
@@ -188,11 +188,13 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
     for (int y = 0; y < 4; ++y) s4[y] = (p[4 * y] + p[4 * y + 1]) + (p[4 * y + 2] + p[4 * y + 3]);
     lsum += (s4[0] + s4[1]) + (s4[2] + s4[3]);
     const float mx = row_max(snext);
-    // A: four K reads up front, then per MFMA one more read and ~5 VALU ops;
-    // no VALU right after the last S^T MFMA (what is left is the row max of
-    // S^T(u+1), which would wait for that MFMA to finish).
+    // A: four K reads and four exponent FMAs up front, then per MFMA one more
+    // read, 16 / NK exps (the scheduling groups count transcendental ops
+    // apart from other VALU ops) and ~4 VALU ops; no VALU right after the
+    // last S^T MFMA (what is left is the row max of S^T(u+1), which would
+    // wait for that MFMA to finish).
     SGB(kSgDSRead, 4);
-    SGB(kSgVALU, 6);
+    SGB(kSgVALU, 4);
 #pragma unroll
     for (int i = 0; i < NK; ++i) {
       SGB(kSgMFMA, 1);
@@ -201,7 +203,8 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(ChunkArgs a) {
       } else {
         SGB(kSgDSRead, 2);
       }
-      if (i < NK - 1) SGB(kSgVALU, 5);
+      SGB(kSgTrans, 16 / NK);
+      if (i < NK - 1) SGB(kSgVALU, 4);
     }
     // B: the first PV MFMA, the remaining V reads, then the other PV MFMAs
     // with the sums and the max.

@@ -86,8 +86,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   constexpr int IPWQ = (kSB / T::RPI) / 4;  // DMA instructions per wave per tensor per sub-block
   static_assert(IPWQ >= 1 && IPWQ * 4 * T::RPI == kSB, "sub-block splits over 4 waves");
   constexpr int DMA_PER_SB = 2 * IPWQ + 1;  // Q, dO, and one for the [LSE2 | -Delta] record
-  // One LDS object per ring slot: [Q rows | dO rows | LSE2 (32 floats) | -Delta (32 floats)].
-  constexpr int SLOT = 2 * kSB * P + 128;
+  // One LDS object per ring slot, [Q rows | dO rows], and the slots' records,
+  // [LSE2 (32 floats) | -Delta (32 floats)], in an array of their own at the
+  // bottom of LDS, where the broadcast reads take their offsets as immediates.
+  constexpr int SLOT = 2 * kSB * P;
+  __shared__ __attribute__((aligned(1024))) float REC[kRing][64];
   __shared__ __attribute__((aligned(1024))) uint16_t R0[SLOT], R1[SLOT], R2[SLOT], R3[SLOT], R4[SLOT], R5[SLOT];
   auto slot = [&](auto I) -> uint16_t* {
     constexpr int i = decltype(I)::value;
@@ -96,7 +99,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
   };
   auto qbuf = [&](auto I) -> uint16_t* { return slot(I); };
   auto obuf = [&](auto I) -> uint16_t* { return slot(I) + kSB * P; };
-  auto lbuf = [&](auto I) -> float* { return reinterpret_cast<float*>(slot(I) + 2 * kSB * P); };
+  auto lbuf = [&](auto I) -> float* { return REC[decltype(I)::value]; };
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, g = lane >> 5;

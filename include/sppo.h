@@ -88,7 +88,7 @@ typedef enum {
  * shape (query heads, KV heads, head dim).  Copied by sppo_create. */
 typedef struct {
   int64_t batch;                 /* B >= 1                                  */
-  int64_t seq_len;               /* S >= 1                                  */
+  int64_t seq_len;               /* 1 <= S < 2^31 (kernels index keys in int) */
   int32_t n_chunks;              /* N, 1 <= N <= S                          */
   const int64_t* chunk_offsets;  /* host array of N+1 offsets, strictly
                                     increasing from 0 to S; NULL means N

@@ -284,12 +284,14 @@ void destroy_all(sppo_ctx* c) {
       if (e) (void)hipEventDestroy(e);
     }
   }
-  for (auto* v : {&c->t_d2h, &c->t_h2d, &c->t_h2d_kv, &c->t_kern[0], &c->t_kern[1], &c->t_kern[2], &c->t_kern[3]}) {
-    for (EventPair& p : *v) {
+  auto destroy_pairs = [](std::vector<EventPair>& v) {
+    for (EventPair& p : v) {
       if (p.start) (void)hipEventDestroy(p.start);
       if (p.stop) (void)hipEventDestroy(p.stop);
     }
-  }
+  };
+  for (auto* v : {&c->t_d2h, &c->t_h2d, &c->t_h2d_kv}) destroy_pairs(*v);
+  for (auto& v : c->t_kern) destroy_pairs(v);
   for (HostSlot& s : c->slots) {
     if (s.base) (void)hipHostFree(s.base);
   }
@@ -328,6 +330,9 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
   }
   if (p->n_q_heads < 1 || p->n_kv_heads < 1 || p->n_q_heads % p->n_kv_heads != 0) {
     return fail(nullptr, SPPO_ERR_INVALID_ARG, "need n_q_heads a positive multiple of n_kv_heads");
+  }
+  if (p->seq_len > 0x7fffffff) {
+    return fail(nullptr, SPPO_ERR_UNSUPPORTED, "seq_len of 2^31 or more is not supported");
   }
   if (p->n_q_heads > 65535 || p->n_kv_heads > 65535 || p->batch > 65535) {
     return fail(nullptr, SPPO_ERR_UNSUPPORTED, "batch and head counts above 65535 are not supported");

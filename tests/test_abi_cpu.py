@@ -37,6 +37,7 @@ GOOD = dict(batch=1, seq_len=1024, n_chunks=4, n_q_heads=8, n_kv_heads=2, head_d
 @pytest.mark.parametrize("change,status", [
     (dict(head_dim=96), L.SPPO_ERR_UNSUPPORTED),
     (dict(head_dim=0), L.SPPO_ERR_UNSUPPORTED),
+    (dict(seq_len=2**31, n_chunks=1), L.SPPO_ERR_UNSUPPORTED),   # key indices are int32
     (dict(n_kv_heads=3), L.SPPO_ERR_INVALID_ARG),
     (dict(n_kv_heads=0), L.SPPO_ERR_INVALID_ARG),
     (dict(batch=0), L.SPPO_ERR_INVALID_ARG),

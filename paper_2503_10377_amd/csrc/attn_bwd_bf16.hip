@@ -504,9 +504,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, g = lane >> 5;
-  const int t = gridDim.x - 1 - blockIdx.x;  // longest (latest) query tiles first
-  const int h = blockIdx.y;
-  const int64_t b = blockIdx.z;
+  const GridPos gp = xcd_grouped();  // the query tiles of a head behind one L2
+  const int t = gridDim.x - 1 - gp.x;  // longest (latest) query tiles first
+  const int h = gp.y;
+  const int64_t b = gp.z;
   const int hk = h / (a.Hq / a.Hkv);
   const int64_t c0 = a.c0, c1 = a.c1, s = c1 - c0;
   const int64_t q0 = c0 + (int64_t)t * kDqRows;

@@ -116,6 +116,24 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(uint64_t addr, in
                                            __builtin_amdgcn_readfirstlane(nbytes), kBufferFlags);
 }
 
+// ------------------------------------------------------- XCD grouping
+// The dispatcher hands workgroups to the 8 XCDs (each with its own L2)
+// round-robin in linear order (x fastest).  xcd_grouped() returns the grid
+// position a workgroup works on such that each XCD receives one contiguous
+// range of linear positions: the query tiles of one head, which all stream
+// the same K/V rows, then run side by side behind one L2.  A grid whose size
+// is not a multiple of 8 keeps the identity mapping.
+struct GridPos {
+  int x, y, z;
+};
+__device__ __forceinline__ GridPos xcd_grouped() {
+  const uint32_t nx = gridDim.x, ny = gridDim.y;
+  const uint32_t total = nx * ny * gridDim.z;
+  uint32_t n = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+  if (total % 8 == 0) n = (n % 8) * (total / 8) + n / 8;
+  return GridPos{(int)(n % nx), (int)((n / nx) % ny), (int)(n / (nx * ny))};
+}
+
 // ------------------------------------------------------------- LDS-DMA
 // buffer_load ... lds moves 16 (or 4) bytes per lane from a buffer resource
 // straight into LDS, lane l's bytes landing at lds + 16 l (4 l): one wave

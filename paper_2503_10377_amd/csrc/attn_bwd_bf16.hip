@@ -103,12 +103,13 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, g = lane >> 5;
-  const int hk = blockIdx.y;
-  const int64_t b = blockIdx.z;
+  const GridPos gp = xcd_grouped();  // the key blocks of a KV head behind one L2
+  const int hk = gp.y;
+  const int64_t b = gp.z;
   const int G = a.Hq / a.Hkv;
   const int64_t c0 = a.c0, c1 = a.c1, s = c1 - c0;
   const int64_t kv1 = a.kv1;
-  const int64_t k0 = a.kv0 + (int64_t)blockIdx.x * kKvKeys;
+  const int64_t k0 = a.kv0 + (int64_t)gp.x * kKvKeys;
   const int64_t j = k0 + 32 * w + l32;  // this lane's key
   const float C = a.scale * kLog2e;
 

@@ -79,14 +79,33 @@ def algorithmic_flops(offsets, B, Hq, D):
 
 
 def cpu_model():
+    """The host CPU as /proc/cpuinfo names it: model name, family, model and
+    stepping, and the number of logical CPUs it lists."""
+    fields, n = {}, 0
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                key, _, val = line.partition(":")
+                key = key.strip()
+                if key == "processor":
+                    n += 1
+                if key in ("model name", "cpu family", "model", "stepping", "vendor_id") and key not in fields:
+                    fields[key] = val.strip()
     except OSError:
-        pass
-    return "unknown"
+        return "unknown"
+    return (f"{fields.get('model name', 'unknown')} ({fields.get('vendor_id', '?')}, family "
+            f"{fields.get('cpu family', '?')} model {fields.get('model', '?')} stepping "
+            f"{fields.get('stepping', '?')}; {n} logical CPUs listed)")
+
+
+def cpu_threads():
+    """Host threads for the oracle: the CPUs this process may run on, capped
+    by the OpenMP thread limit of the environment (the CPU share of one GPU
+    on a shared box), and the affinity count itself."""
+    affinity = len(os.sched_getaffinity(0))
+    cap = os.environ.get("OMP_NUM_THREADS", "")
+    n = min(affinity, int(cap)) if cap.isdigit() and int(cap) > 0 else affinity
+    return n, affinity
 
 
 def oracle_cpu_baseline(inp, D, sample_tokens, sample_heads):
@@ -100,18 +119,17 @@ def oracle_cpu_baseline(inp, D, sample_tokens, sample_heads):
     def host(t):
         return t[:, :sample_tokens, :sample_heads].float().cpu().numpy().astype(np.float64)
 
+    from threadpoolctl import threadpool_limits
+
     q, k, v, do = host(inp["q"]), host(inp["k"]), host(inp["v"]), host(inp["do"])
-    try:
-        from threadpoolctl import threadpool_info
-        info = threadpool_info()
-        cores = max(i.get("num_threads", 1) for i in info) if info else 1
-    except Exception:
-        cores = len(os.sched_getaffinity(0))
-    t0 = time.perf_counter()
-    oracle.attention(q, k, v, do, 1.0 / math.sqrt(D))
-    dt = time.perf_counter() - t0
+    cores, affinity = cpu_threads()
+    with threadpool_limits(cores):
+        t0 = time.perf_counter()
+        oracle.attention(q, k, v, do, 1.0 / math.sqrt(D))
+        dt = time.perf_counter() - t0
     flops = 14 * D * sample_heads * sample_tokens * (sample_tokens + 1) / 2
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "affinity_cpus": affinity,
             "sample": f"fp64 NumPy oracle, unchunked fwd+bwd of heads 0..{sample_heads - 1} over the "
                       f"first {sample_tokens} tokens ({flops:.3e} algorithmic flop in {dt:.2f} s)",
             "seconds": dt}
@@ -171,7 +189,7 @@ def sweep_chunk_count(args, inp, S, Hq, Hkv, D, counts):
         row = {"sweep": "chunk_count", "seq_len": S, "n_chunks": n, "chunk_len": S // n, "n_q_heads": Hq,
                "n_kv_heads": Hkv, "head_dim": D, "steps": args.steps}
         for phase, run in (("fwd", lambda: ca.forward_only(inp, out)),
-                           ("fwd_bwd", lambda: ca.step(inp, out))):
+                           ("fwd_bwd", lambda: ca.step(inp, out, export=False))):
             for _ in range(args.warmup):
                 run()
             torch.cuda.synchronize()
@@ -204,18 +222,17 @@ def layer_cpu_baseline(inp, p, Hq, Hkv, D, sample_tokens):
     host = lambda t: t.float().cpu().numpy().astype(np.float64)
     x, dy = host(inp["x"][:sample_tokens]), host(inp["dy"][:sample_tokens])
     hp = {k: host(v) for k, v in p.items()}
-    try:
-        from threadpoolctl import threadpool_info
-        info = threadpool_info()
-        cores = max(i.get("num_threads", 1) for i in info) if info else 1
-    except Exception:
-        cores = len(os.sched_getaffinity(0))
+    from threadpoolctl import threadpool_limits
+
     from paper_2503_10377_amd.chunked_layer import ChunkedLayer
+    cores, affinity = cpu_threads()
     flops, _ = ChunkedLayer.flops(sample_tokens, [0, sample_tokens], Hq, Hkv, D)
-    t0 = time.perf_counter()
-    T.layer(x, dy, hp, Hq, Hkv, D)
-    dt = time.perf_counter() - t0
+    with threadpool_limits(cores):
+        t0 = time.perf_counter()
+        T.layer(x, dy, hp, Hq, Hkv, D)
+        dt = time.perf_counter() - t0
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "affinity_cpus": affinity,
             "sample": f"fp64 NumPy layer oracle, unchunked fwd+bwd of the full layer over the first "
                       f"{sample_tokens} tokens ({flops:.3e} algorithmic flop in {dt:.2f} s)"}
 
@@ -391,7 +408,7 @@ def main():
         sweep_chunk_count(args, inp, S, Hq, Hkv, D, [int(x) for x in args.sweep_n.split(",")])
         return
     ca = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload=offload)
-    out = ca.alloc_outputs()
+    out = ca.alloc_outputs(export=False)
     flops = algorithmic_flops(ca.offsets, B, Hq, D)
 
     def timed(c, steps, timing, o=None):
@@ -428,6 +445,20 @@ def main():
         span = {marks[n][0]: marks[n][1].elapsed_time(marks[n + 1][1]) for n in range(len(marks) - 1)}
         return [span[("fwd", i)] for i in range(c.N)]
 
+    def device_memory(c, o):
+        """Measured device memory of one walk: torch's peak of allocated
+        bytes over a step (inputs, outputs and the walk's buffers), and the
+        bytes the walk holds for the chunks' saved activations (its device
+        arena and keep buffers, allocated before the walk)."""
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        c.step(inp, o, lookahead=args.lookahead)
+        torch.cuda.synchronize()
+        return {"peak_allocated_GiB": torch.cuda.max_memory_allocated() / 2**30,
+                "saved_activation_GiB": (c.arena.nbytes + c.keep.nbytes) / 2**30,
+                "arena_GiB": c.arena.nbytes / 2**30, "keep_GiB": c.keep.nbytes / 2**30,
+                "arena_high_water_GiB": c.arena.high_water / 2**30}
+
     def modelled_peak_bytes(t_fwd, lens, rows, copy_row, freed_row, bw_GBps):
         """Peak device bytes of the chunks' offloadable activations (Q, O,
         LSE) during the forward walk, when each offloaded prefix is freed as
@@ -461,15 +492,17 @@ def main():
         for part in ("equal", "balanced"):
             offs = None if part == "equal" else L.sppo_balanced_offsets(S, N, 128)
             c_none = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offsets=offs, offload="none")
-            o = c_none.alloc_outputs()
+            o = c_none.alloc_outputs(export=False)
             ms_none, _, _ = timed(c_none, steps, False, o)
             t_fwd = chunk_fwd_ms(c_none, o)
+            mem_none = device_memory(c_none, o)
             c_none.close()
             c_on = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offsets=offs, offload="qkvol")
             lens = [c_on.chunk_len(i) for i in range(N)]
             copy_row = c_on.offload_bytes_per_row()
             plan = L.sppo_plan_offload_rows(c_on.offsets, copy_row, bw_GBps, t_fwd[1:] + [0.0], 128)
-            entry = {"offsets": c_on.offsets, "ms_per_step_no_offload": ms_none, "fwd_ms_per_chunk": t_fwd}
+            entry = {"offsets": c_on.offsets, "ms_per_step_no_offload": ms_none, "fwd_ms_per_chunk": t_fwd,
+                     "device_memory_no_offload": mem_none}
             for name, rows in (("full", lens[:-1] + [0]), ("plan", plan)):
                 c_on.set_offload_rows(rows)
                 ms, _, cs_p = timed(c_on, steps, False, o)
@@ -482,7 +515,8 @@ def main():
                     "exposed_ms_per_step": exp_p,
                     "hidden_pct": 100.0 * max(0.0, min(1.0, 1.0 - exp_p / copy_p)) if copy_p > 0 else None,
                     "modelled_peak_activation_GiB": modelled_peak_bytes(
-                        t_fwd, lens, rows, copy_row, freed_row, bw_GBps) / 2**30}
+                        t_fwd, lens, rows, copy_row, freed_row, bw_GBps) / 2**30,
+                    "device_memory": device_memory(c_on, o)}
             c_on.close()
             result[part] = entry
             print(f"[bench] policy {part}: full {entry['full']['ms_per_step']:.1f} ms, "
@@ -516,7 +550,9 @@ def main():
     res["config"] = {
         "workload": f"chunked causal attention fwd+bwd, batch {B}, seq {S} in {N} chunks of {S // N}, "
                     f"{Hq} query / {Hkv} KV heads x head_dim {D}, bf16 in / fp32 accumulate, "
-                    f"offload {offload} (all chunks but the last), prefetch lookahead {args.lookahead}",
+                    f"offload {offload} (all chunks but the last), prefetch lookahead {args.lookahead}"
+                    + (" (Q/O/LSE offloaded and prefetched back through a device ring; K/V copied to the "
+                       "host only, the K/V cache stays resident)" if offload == "qkvol" else ""),
         "name": args.workload, "batch": B, "seq_len": S, "n_chunks": N, "n_q_heads": Hq,
         "n_kv_heads": Hkv, "head_dim": D, "offload": offload,
     }
@@ -532,18 +568,26 @@ def main():
     res["kernels"] = kern
     dom = max((n for n in kern if flops.get(n)), key=lambda n: kern[n]["ms_per_step"])
     ach = kern[dom]["tflops"]
+    traffic = measured_traffic(dom, args.workload)
     res["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
-                       "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS,
-                       "traffic": measured_traffic(dom, args.workload)}
+                       "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": traffic,
+                       "traffic_source": (f"profiles/{dom}_{args.workload}_traffic.json: FETCH_SIZE + WRITE_SIZE "
+                                          "from separate rocprofv3 --pmc runs of this command, scaled by a 1 GiB "
+                                          "copy, kept only while the kernel source's sha256 matches (not "
+                                          "measured in this run)") if traffic is not None else None}
     if cs is not None:
         copy_ms = (cs["ms_d2h"] + cs["ms_h2d"]) / steps
         off = {"bytes_d2h_per_step": cs["bytes_d2h"] / steps, "bytes_h2d_per_step": cs["bytes_h2d"] / steps,
                "copy_ms_per_step": copy_ms,
                "d2h_GBps": cs["bytes_d2h"] / max(cs["ms_d2h"], 1e-9) / 1e6,
                "h2d_GBps": cs["bytes_h2d"] / max(cs["ms_h2d"], 1e-9) / 1e6}
+        off["kv_copy_only"] = offload == "qkvol"
         if not args.no_offload_compare:
             ca_off = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="none")
             ms_off, _, _ = timed(ca_off, steps, False)
+            off["device_memory"] = {"offload": device_memory(ca, out), "no_offload": device_memory(ca_off, out)}
+            off["device_memory"]["saved_GiB"] = (off["device_memory"]["no_offload"]["peak_allocated_GiB"] -
+                                                 off["device_memory"]["offload"]["peak_allocated_GiB"])
             # Per-chunk exposed time: one more step of each with an event at
             # every chunk boundary; exposed = duration with offload minus
             # duration without, per forward and per backward chunk.
@@ -561,6 +605,19 @@ def main():
             off["exposed_ms_per_step"] = exposed
             off["hidden_pct"] = 100.0 * max(0.0, min(1.0, 1.0 - exposed / copy_ms)) if copy_ms > 0 else None
             if offload == "qkvol":
+                # The round-trip set alone: Q/O/LSE go out and come back, K/V
+                # are not copied at all (in the headline walk they are copied
+                # to the host and never needed back).
+                ca_q = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="qol")
+                ms_q, _, cs_q = timed(ca_q, steps, False)
+                ca_q.close()
+                copy_q = (cs_q["ms_d2h"] + cs_q["ms_h2d"]) / steps
+                exp_q = max(0.0, ms_q - ms_off)
+                off["round_trip_qol"] = {
+                    "ms_per_step": ms_q, "bytes_d2h_per_step": cs_q["bytes_d2h"] / steps,
+                    "bytes_h2d_per_step": cs_q["bytes_h2d"] / steps, "copy_ms_per_step": copy_q,
+                    "exposed_ms_per_step": exp_q,
+                    "hidden_pct": 100.0 * max(0.0, min(1.0, 1.0 - exp_q / copy_q)) if copy_q > 0 else None}
                 # The same walk with the K/V cache rows given up after the
                 # forward and streamed back under the last chunk's backward.
                 ca_ev = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="qkvol_evict")
@@ -589,7 +646,7 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         cb = oracle_cpu_baseline(inp, D, args.cpu_sample_tokens, args.cpu_sample_heads)
-        res["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+        res["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample", "affinity_cpus")}
         res["cpu_baseline"]["cpu_model"] = cpu_model()
         # an extrapolation from the measured rate, not a measurement
         res["cpu_baseline"]["extrapolated_full_step_s"] = flops["total"] / (cb["value"] * 1e12)

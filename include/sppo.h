@@ -118,6 +118,21 @@ typedef struct {
   void* v;      /* base of the full V cache [B, S, Hkv, D]; rows of chunk i  */
   void* const* extra; /* n_extra device pointers (planes of chunk i), or
                          NULL when the problem has no extra planes          */
+  void* keep;   /* device buffer of sppo_keep_bytes(ctx, i) bytes, 16-byte
+                   aligned, or NULL.  With sequence-aware offloading (rows_i
+                   < s_i, see sppo_set_offload_rows) the rows [rows_i, s_i)
+                   of Q_i, O_i, LSE_i and the extra planes stay on the
+                   device.  With a keep buffer, sppo_offload_issue moves
+                   them there (a device-to-device copy on its stream), so
+                   the source buffers are dead as a whole after
+                   sppo_offload_wait and can be reused (a device staging
+                   ring), and sppo_prefetch moves them back into its
+                   destination buffers (on its stream) -- pass the same
+                   keep pointer to both.  Without one, they stay in the
+                   source buffers, and the prefetch must target those same
+                   buffers.  Ignored when rows_i == s_i.  The caller owns
+                   the buffer and keeps it untouched from the offload to
+                   the prefetch of chunk i.                                 */
 } sppo_chunk_bufs;
 
 typedef struct {
@@ -253,8 +268,27 @@ sppo_status sppo_plan_offload_rows(const int64_t* offsets, int32_t n_chunks, dou
                                    double bw_GBps, const double* t_overlap_ms, int64_t align,
                                    int64_t* rows_out);
 
+/* Bytes of chunk i's keep buffer (see sppo_chunk_bufs.keep) for its
+ * current offload row count: 0 when the whole chunk is offloaded, or for an
+ * invalid context or index. */
+size_t sppo_keep_bytes(const sppo_ctx* ctx, int32_t i);
+
+/* Finalize step of the reverse walk (optional): key j receives gradient
+ * only from query rows r >= j, and the walk runs the backward of chunks
+ * N-1, ..., 0 (Sec. 5.2), so once bwd(i) has been issued the dK/dV rows
+ * [c_i, c_{i+1}) are final.  Writes those rows of every batch entry of
+ * dk_out/dv_out ([B, S, Hkv, D] in the problem's dtype: fp32 accumulators
+ * rounded to nearest even for bf16, copied for fp32) on `stream`, after
+ * the backward enqueued there.  Rows outside the chunk are not touched.
+ * Errors: STATE (bwd(i) not issued since the last fwd(0) or reset),
+ * INVALID_ARG (null/misaligned pointers, dk_out == dv_out). */
+sppo_status sppo_attn_finalize_chunk(sppo_ctx* ctx, int32_t i, const float* dk_acc, const float* dv_acc,
+                                     void* dk_out, void* dv_out, void* stream);
+
 /* Abandon the current forward/backward walk (e.g. after a forward-only run):
- * the next call must be fwd(0).  Clears per-chunk offload state. */
+ * the next call must be fwd(0).  Blocks until the context's copy streams
+ * are idle (copies of the abandoned walk may still read or write its
+ * device buffers and host slots), then clears per-chunk offload state. */
 sppo_status sppo_reset(sppo_ctx* ctx);
 
 /* Block until the context's copy streams are idle. */

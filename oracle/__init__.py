@@ -28,6 +28,7 @@ from .causal_attention import (  # noqa: F401
     equal_offsets,
     rows_fwd_bwd,
     tail_keys_bwd,
+    keys_bwd_rows,
 )
 from .transformer_layer import (  # noqa: F401
     chunked_layer,

@@ -278,3 +278,50 @@ def tail_keys_bwd(q_tail, do_tail, k, v, scale, t0, row_block=256):
                     dk[b, :, g, :] += scale * (ds.T @ qb)
                     dv[b, :, g, :] += pt.T @ dob
     return dk, dv
+
+
+def keys_bwd_rows(q_rows, do_rows, row0, k, v, scale, keys, row_block=256):
+    """Contributions of the query rows [row0, row0 + R) to dK/dV at selected
+    keys.
+
+    dK_j and dV_j are sums over the rows r >= j (the backward formulas in the
+    module docstring), and each row's terms need only that row's own LSE and
+    Delta, formed here from all of its keys 0..r exactly as in
+    ``attention_fwd`` / ``attention_bwd``.  Rows are independent, so summing
+    this function over a partition of the rows [min(keys), S) gives the
+    exact dK/dV at ``keys``: the chunked backward walk (Sec. 5.2) adds the
+    same terms, chunk by chunk in reverse order, for the early keys that
+    accumulate over many backward calls.
+
+    q_rows, do_rows : Q and dO rows [row0, row0 + R) as [B, R, Hq, D]
+    k, v            : the full [B, S, Hkv, D] (any float dtype)
+    keys            : global key indices (any order, may repeat)
+    Returns (dk, dv) as [B, len(keys), Hkv, D]."""
+    q_rows, do_rows = _f64(q_rows), _f64(do_rows)
+    keys = np.asarray(keys, dtype=np.int64)
+    B, R, Hq, D = q_rows.shape
+    Hkv = k.shape[2]
+    G = _group(Hq, Hkv)
+    dk = np.zeros((B, len(keys), Hkv, D))
+    dv = np.zeros((B, len(keys), Hkv, D))
+    rmax = row0 + R
+    for b in range(B):
+        for g in range(Hkv):
+            kg, vg = _f64(k[b, :rmax, g, :]), _f64(v[b, :rmax, g, :])
+            k_sel, v_sel = kg[np.minimum(keys, rmax - 1)], vg[np.minimum(keys, rmax - 1)]
+            for h in range(g * G, (g + 1) * G):
+                for a0 in range(0, R, row_block):
+                    a1 = min(R, a0 + row_block)
+                    rows = np.arange(row0 + a0, row0 + a1)
+                    r_end = row0 + a1
+                    qb, dob = q_rows[b, a0:a1, h, :], do_rows[b, a0:a1, h, :]
+                    s = _masked_scores(qb, kg[:r_end], scale, rows, np.arange(r_end))
+                    l_ = _row_lse(s)
+                    delta = (dob * (np.exp(s - l_) @ vg[:r_end])).sum(axis=1)
+                    # the selected keys' columns: s_rj and P_rj, zero where j > r
+                    s_sel = scale * (qb @ k_sel.T)
+                    p_sel = np.where(keys[None, :] <= rows[:, None], np.exp(s_sel - l_), 0.0)
+                    ds = p_sel * (dob @ v_sel.T - delta[:, None])
+                    dk[b, :, g, :] += scale * (ds.T @ qb)
+                    dv[b, :, g, :] += p_sel.T @ dob
+    return dk, dv

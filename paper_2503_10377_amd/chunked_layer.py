@@ -17,6 +17,12 @@ LayerNorms' statistics -- is offloaded after the chunk's forward (all chunks
 but the last by default) and prefetched before its backward.  u, z and
 gelu(a) are recomputed in the backward from x, h and a.
 
+The saved tensors a chunk produces live in a region of a preallocated
+device arena (ring.DeviceArena): an offloaded chunk's region is reused once
+its copy has landed, and its prefetch lands in a free region.  x_i is read
+from the caller's x in the forward (those rows of x are dead once
+offloaded) and comes back into the chunk's region.
+
 The host stays at most ``host_ahead`` chunk boundaries ahead of the device
 (a HostPacer; 0 lets it run free).
 
@@ -29,13 +35,14 @@ import torch
 
 from . import sppo as L
 from .pacing import HostPacer
+from .ring import DeviceArena, KeepArena, plan_capacity, plane_layout, walk_schedule
 
 PLANES = ("x", "h", "a", "m1", "r1", "m2", "r2")
 
 
 class ChunkedLayer:
     def __init__(self, S, n_chunks, Hq, Hkv, D, offsets=None, offload="none", device="cuda", eps=1e-5,
-                 host_ahead=2):
+                 host_ahead=2, fwd_slots=4):
         H = Hq * D
         wt = (Hq + 2 * Hkv) * D
         if H % 256 or wt % 256 or H > 8192:
@@ -50,6 +57,10 @@ class ChunkedLayer:
         self.offload = L.OFFLOAD_MODES.get(offload, offload)
         self.s_max = max(self.offsets[i + 1] - self.offsets[i] for i in range(n_chunks))
         self.pacer = HostPacer(host_ahead)
+        self.fwd_slots = fwd_slots
+        self.arena = None
+        self.keep = None
+        self._layout = None
         self._alloc()
 
     def close(self):
@@ -63,23 +74,9 @@ class ChunkedLayer:
         bf, f32 = torch.bfloat16, torch.float32
         HqD, HkvD, sm = self.Hq * self.D, self.Hkv * self.D, self.s_max
         e = lambda *shape, dt=bf: torch.empty(*shape, dtype=dt, device=dev)
-        # saved activations (chunk views of full-length buffers)
-        self.q, self.o = e(S, HqD), e(S, HqD)
-        self.h, self.a = e(S, H), e(S, 4 * H)
+        # the K/V cache and its gradient accumulators (full length)
         self.k, self.v = e(S, HkvD), e(S, HkvD)
         self.dk, self.dv = e(S, HkvD, dt=f32), e(S, HkvD, dt=f32)
-        # per-chunk fp32 rows (LSE [Hq, s_i] and the four LayerNorm statistics),
-        # each chunk's slot starting on a 16-byte boundary
-        def slots(n_per_row):
-            sizes = [n_per_row * self.chunk_len(i) for i in range(self.N)]
-            flat = torch.empty(sum((n + 3) // 4 * 4 for n in sizes), dtype=f32, device=dev)
-            out, pos = [], 0
-            for n in sizes:
-                out.append(flat[pos:pos + n])
-                pos += (n + 3) // 4 * 4
-            return out
-        self.lse = [t.view(self.Hq, -1) for t in slots(self.Hq)]
-        self.stats = {name: slots(1) for name in ("m1", "r1", "m2", "r2")}
         # transposed weights for the forward GEMMs
         self.wT = {"w_qkv": e(Wt, H), "w_o": e(H, HqD), "w_1": e(4 * H, H), "w_2": e(H, 4 * H)}
         # chunk-sized scratch
@@ -114,21 +111,57 @@ class ChunkedLayer:
             L.sppo_set_offload_rows(self.ctx, i, r)
 
     # ------------------------------------------------------------ the walk
-    def _views(self, x, i):
-        c0, c1 = self.offsets[i], self.offsets[i + 1]
-        return dict(x=x[c0:c1], q=self.q[c0:c1], o=self.o[c0:c1], h=self.h[c0:c1], a=self.a[c0:c1],
-                    lse=self.lse[i], **{k: self.stats[k][i] for k in ("m1", "r1", "m2", "r2")})
+    def region_planes(self, i):
+        """Byte sizes of chunk i's saved tensors in its arena region."""
+        n, H, HqD = self.chunk_len(i), self.H, self.Hq * self.D
+        return {"q": 2 * n * HqD, "o": 2 * n * HqD, "lse": 4 * self.Hq * n, "x": 2 * n * H, "h": 2 * n * H,
+                "a": 8 * n * H, "m1": 4 * n, "r1": 4 * n, "m2": 4 * n, "r2": 4 * n}
 
-    def _bufs(self, v):
+    def prepare(self, offload_chunks, lookahead):
+        """Allocate the device arena and keep buffers for a walk with these
+        settings (again only when they change; a walk allocates nothing).
+        Returns the bytes they hold."""
+        offl = tuple(sorted(set(offload_chunks)))
+        key = (offl, lookahead, tuple(L.sppo_get_offload_rows(self.ctx)))
+        if self._layout != key:
+            self._planes = [plane_layout(self.region_planes(i)) for i in range(self.N)]
+            q = self.fwd_slots - 1
+            cap, q = plan_capacity(walk_schedule(self.N, offl, lookahead), [sz for _, sz in self._planes],
+                                   quarantine=q)
+            self.arena = None
+            self.keep = None
+            self.arena = DeviceArena(cap, self.device, quarantine=q)
+            self.keep = KeepArena([L.sppo_keep_bytes(self.ctx, i) if i in offl else 0 for i in range(self.N)],
+                                  self.device)
+            self._layout = key
+        return self.arena.nbytes + self.keep.nbytes
+
+    def _acquire(self, i, s, x=None):
+        """Allocate chunk i's region; returns (offset, views of its saved
+        tensors).  x_i is the caller's rows when given, else the region's x
+        plane (where a prefetch puts it)."""
+        off = self.arena.acquire(self.ctx, s, self._planes[i][1], i)
+        n, H, HqD = self.chunk_len(i), self.H, self.Hq * self.D
+        bf, f32 = torch.bfloat16, torch.float32
+        po = self._planes[i][0]
+        pl = lambda name, shape, dt: self.arena.view(off + po[name], shape, dt)  # noqa: E731
+        v = dict(q=pl("q", (n, HqD), bf), o=pl("o", (n, HqD), bf), lse=pl("lse", (self.Hq, n), f32),
+                 h=pl("h", (n, H), bf), a=pl("a", (n, 4 * H), bf),
+                 **{k: pl(k, (n,), f32) for k in ("m1", "r1", "m2", "r2")})
+        v["x"] = x if x is not None else pl("x", (n, H), bf)
+        return off, v
+
+    def _bufs(self, v, keep):
         return L.chunk_bufs(q=v["q"], o=v["o"], lse=v["lse"], k=self.k, v=self.v,
-                            extra=[v[name] for name in PLANES])
+                            extra=[v[name] for name in PLANES], keep=keep)
 
     def step(self, inp, p, out, offload_chunks=None, lookahead=2, poison=False, stream=None, marks=None,
              ops=None):
         """Forward and backward of the layer over all chunks.  inp: x, dy
         [S, H] bf16 (x's chunk rows are the x planes: offloading a chunk
-        makes its rows of x dead until the prefetch; poison=True overwrites
-        them, and every other offloaded row, with NaN once copied).  p: the
+        makes its rows of x dead, and the prefetch brings them back into the
+        chunk's arena region; poison=True overwrites every dead buffer -- the
+        rows of x and the chunk's region -- with NaN once copied).  p: the
         weights (w_qkv, w_o, w_1, w_2 bf16; g1, b1, g2, b2 fp32).  marks:
         list that receives ((phase, chunk), event) at every chunk boundary.
         ops: list that receives (category, algorithmic flop, start event,
@@ -138,7 +171,9 @@ class ChunkedLayer:
         if offload_chunks is None:
             offload_chunks = [] if self.offload == L.SPPO_OFFLOAD_NONE else list(range(self.N - 1))
         offl = set(offload_chunks)
-        rows = L.sppo_get_offload_rows(self.ctx) if poison else None
+        self.prepare(offl, lookahead)
+        arena, keep = self.arena, self.keep
+        arena.reset()
         x, dy = inp["x"], inp["dy"]
 
         def mark(label):
@@ -178,9 +213,11 @@ class ChunkedLayer:
         transpose(p["w_o"], self.wT["w_o"], HqD, H, s)
         transpose(p["w_1"], self.wT["w_1"], H, 4 * H, s)
         transpose(p["w_2"], self.wT["w_2"], 4 * H, H, s)
+        held, back = {}, {}  # chunk -> (region, views): not offloaded / prefetched
         for i in range(self.N):
             mark(("fwd", i))
-            n, c0, v = self.chunk_len(i), self.offsets[i], self._views(x, i)
+            n, c0 = self.chunk_len(i), self.offsets[i]
+            slot, v = self._acquire(i, s, x=x[c0:c0 + n])
             u, z, g = self.u[:n], self.z[:n], self.g[:n]
             ln_fwd(n, H, v["x"], H, p["g1"], p["b1"], self.eps, u, H, v["m1"], v["r1"], s)
             wq = self.wT["w_qkv"]
@@ -194,25 +231,30 @@ class ChunkedLayer:
             gemm("nt", n, H, 4 * H, g, 4 * H, self.wT["w_2"], 4 * H, out["y"][c0:], H, "add_bf16", v["h"], H,
                  stream=s)
             if i in offl:
-                L.sppo_offload_issue(self.ctx, i, self._bufs(v), s)
+                L.sppo_offload_issue(self.ctx, i, self._bufs(v, keep.ptr(i)), s)
+                arena.release(slot, after_offload=True)
                 if poison:
-                    # Test hook: once copied, the offloaded rows are dead on the device.
+                    # Test hook: once copied, the chunk's region and its rows of
+                    # x are dead (the rows that stay went to the keep buffer).
                     L.sppo_offload_wait(self.ctx, i, s)
-                    r = rows[i]
                     with torch.cuda.stream(s):
-                        for name in ("x", "q", "o", "h", "a", "m1", "r1", "m2", "r2"):
-                            v[name][:r].fill_(float("nan"))
-                        v["lse"][:, :r].fill_(float("nan"))
+                        for t in v.values():
+                            t.fill_(float("nan"))
+            else:
+                held[i] = (slot, v)
         fwd_phase[0] = False
         pending = sorted(offl, reverse=True)
         nxt = 0
         for i in reversed(range(self.N)):
             while nxt < len(pending) and pending[nxt] >= i - lookahead:
                 j = pending[nxt]
-                L.sppo_prefetch(self.ctx, j, self._bufs(self._views(x, j)), s)
+                slot, vj = self._acquire(j, s)
+                L.sppo_prefetch(self.ctx, j, self._bufs(vj, keep.ptr(j)), s)
+                back[j] = (slot, vj)
                 nxt += 1
             mark(("bwd", i))
-            n, c0, v = self.chunk_len(i), self.offsets[i], self._views(x, i)
+            n, c0 = self.chunk_len(i), self.offsets[i]
+            slot, v = back.pop(i) if i in offl else held.pop(i)
             if i in offl:
                 L.sppo_prefetch_wait(self.ctx, i, s)
             first = i == self.N - 1  # overwrite the weight gradients instead of adding
@@ -245,6 +287,7 @@ class ChunkedLayer:
             ln_bwd(n, H, v["x"], H, p["g1"], v["m1"], v["r1"], self.du[:n], H, dh, H,
                                  out["dx"][c0:], H, out["dg1"], out["db1"], self.ws, self.ws_bytes,
                                  accumulate=0 if first else 1, stream=s)
+            arena.release(slot)
         mark(("end", -1))
 
     @staticmethod

@@ -66,7 +66,12 @@ struct sppo_ctx {
   std::vector<HostSlot> slots;
   std::vector<hipEvent_t> ev_fwd, ev_off, ev_call, ev_pf, ev_kv;
   std::vector<EventPair> t_d2h, t_h2d, t_h2d_kv;
-  std::vector<uint8_t> offloaded, prefetched, kv_prefetched;
+  std::vector<uint8_t> offloaded, prefetched, kv_prefetched, bwd_done;
+  // Where offload_issue(i) left chunk i's rows [rows_i, s_i): in a keep
+  // buffer (keep_ptr[i]), or in the source buffers (src_q[i] etc.), which a
+  // prefetch without a keep buffer must then target.
+  std::vector<void*> keep_ptr, src_q, src_o, src_lse;
+  std::vector<std::vector<void*>> src_extra;
   std::vector<int64_t> rows;  // offloaded row prefix of each chunk (default s_i)
   bool in_bwd = false;
   int next_fwd = 0, next_bwd = -1;
@@ -249,6 +254,52 @@ hipError_t move_kv(sppo_ctx* c, int i, int64_t r, void* k, void* v, bool to_host
   return e;
 }
 
+// Bytes of chunk i's keep buffer: rows [rows_i, s_i) of every tensor of
+// the offload set but K/V (Q_i, O_i, LSE_i, the extra planes), each part
+// starting on a 256-byte boundary.
+size_t keep_bytes(const sppo_ctx* c, int i) {
+  const size_t t = (size_t)(chunk_len(c, i) - c->rows[i]), B = (size_t)c->prob.batch;
+  if (t == 0) return 0;
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t row = (size_t)c->prob.n_q_heads * c->prob.head_dim * c->elt;
+  size_t n = 2 * up(B * t * row) + up(B * c->prob.n_q_heads * t * sizeof(float));
+  for (size_t rb : c->extra_rb) n += up(B * t * rb);
+  return n;
+}
+
+// Device-to-device move of chunk i's rows [r, s_i) between its chunk-local
+// buffers and a keep buffer laid out as [B, s_i - r, ...] per tensor (the
+// order and alignment of keep_bytes).
+hipError_t move_keep(sppo_ctx* c, int i, int64_t r, void* q, void* o, float* lse, void* const* extra, void* keep,
+                     bool to_keep, hipStream_t s) {
+  const size_t si = (size_t)chunk_len(c, i), t = si - (size_t)r, B = (size_t)c->prob.batch;
+  if (t == 0) return hipSuccess;
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t row = (size_t)c->prob.n_q_heads * c->prob.head_dim * c->elt;
+  const hipMemcpyKind kind = hipMemcpyDeviceToDevice;
+  char* kp = static_cast<char*>(keep);
+  hipError_t e = hipSuccess;
+  // [B, s_i, w] plane: B spans of t*w bytes at row r, pitch s_i*w <-> t*w.
+  auto plane = [&](void* dev, size_t w) {
+    char* d = static_cast<char*>(dev) + (size_t)r * w;
+    hipError_t x = to_keep ? copy_rows(kp, t * w, d, si * w, t * w, B, kind, s)
+                           : copy_rows(d, si * w, kp, t * w, t * w, B, kind, s);
+    kp += up(B * t * w);
+    return x;
+  };
+  e = plane(q, row);
+  if (e == hipSuccess) e = plane(o, row);
+  if (e == hipSuccess) {  // LSE_i [B, Hq, s_i]: B*Hq spans of t floats
+    const size_t BH = B * c->prob.n_q_heads;
+    char* d = reinterpret_cast<char*>(lse + r);
+    e = to_keep ? copy_rows(kp, t * 4, d, si * 4, t * 4, BH, kind, s)
+                : copy_rows(d, si * 4, kp, t * 4, t * 4, BH, kind, s);
+    kp += up(BH * t * 4);
+  }
+  for (size_t k = 0; k < c->extra_rb.size() && e == hipSuccess; ++k) e = plane(extra[k], c->extra_rb[k]);
+  return e;
+}
+
 // Fold a finished timing pair into the totals (waits for it if needed).
 void fold(EventPair& p, double& total) {
   if (!p.pending) return;
@@ -422,6 +473,12 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
   c->offloaded.assign(N, 0);
   c->prefetched.assign(N, 0);
   c->kv_prefetched.assign(N, 0);
+  c->bwd_done.assign(N, 0);
+  c->keep_ptr.assign(N, nullptr);
+  c->src_q.assign(N, nullptr);
+  c->src_o.assign(N, nullptr);
+  c->src_lse.assign(N, nullptr);
+  c->src_extra.assign(N, {});
   c->rows.resize(N);
   for (int i = 0; i < N; ++i) c->rows[i] = chunk_len(c, i);
   c->slots.assign(N, HostSlot{});
@@ -500,6 +557,7 @@ sppo_status sppo_attn_fwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i, const
     std::fill(ctx->offloaded.begin(), ctx->offloaded.end(), 0);
     std::fill(ctx->prefetched.begin(), ctx->prefetched.end(), 0);
     std::fill(ctx->kv_prefetched.begin(), ctx->kv_prefetched.end(), 0);
+    std::fill(ctx->bwd_done.begin(), ctx->bwd_done.end(), 0);
   }
   if (++ctx->next_fwd == ctx->prob.n_chunks) {
     ctx->in_bwd = true;
@@ -576,6 +634,7 @@ sppo_status sppo_attn_bwd_chunk(sppo_ctx* ctx, int32_t i, const void* q_i, const
     });
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "backward kernel launch");
+  ctx->bwd_done[i] = 1;
   if (--ctx->next_bwd < 0) {
     ctx->in_bwd = false;
     ctx->next_fwd = 0;
@@ -598,12 +657,27 @@ sppo_status sppo_offload_issue(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* 
   if (!fwd_done) return fail(ctx, SPPO_ERR_STATE, "offload of chunk " + std::to_string(i) + " before its forward");
   if (ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " already offloaded");
 
+  const int64_t r = ctx->rows[i];
+  const bool has_rest = r < chunk_len(ctx, i);
+  if (has_rest && src->keep && !aligned16(src->keep)) {
+    return fail(ctx, SPPO_ERR_INVALID_ARG, "src.keep is not 16-byte aligned");
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  // Rows [r, s_i) stay on the device: into the keep buffer, on the caller's
+  // stream, so the source buffers are free as a whole after E_off[i].
+  if (has_rest && src->keep) {
+    SPPO_HIP(ctx, move_keep(ctx, i, r, src->q, src->o, src->lse, src->extra, src->keep, true, s));
+  }
+  ctx->keep_ptr[i] = has_rest ? src->keep : nullptr;
+  ctx->src_q[i] = src->q;
+  ctx->src_o[i] = src->o;
+  ctx->src_lse[i] = src->lse;
+  ctx->src_extra[i].assign(src->extra ? src->extra : nullptr,
+                           src->extra ? src->extra + ctx->extra_rb.size() : nullptr);
   fold(ctx->t_d2h[i], ctx->ms_d2h);
   SPPO_HIP(ctx, hipEventRecord(ctx->ev_fwd[i], s));
   SPPO_HIP(ctx, hipStreamWaitEvent(ctx->d2h, ctx->ev_fwd[i], 0));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_d2h[i].start, ctx->d2h));
-  const int64_t r = ctx->rows[i];
   uint64_t bytes = 0, kv_bytes = 0;
   SPPO_HIP(ctx, move_qol(ctx, i, r, src->q, src->o, src->lse, src->extra, true, ctx->d2h, &bytes));
   if (offload_kv(ctx)) SPPO_HIP(ctx, move_kv(ctx, i, r, src->k, src->v, true, ctx->d2h, &kv_bytes));
@@ -637,14 +711,34 @@ sppo_status sppo_prefetch(sppo_ctx* ctx, int32_t i, const sppo_chunk_bufs* dst, 
   if ((st = check_extra(ctx, dst->extra, "dst.extra")) != SPPO_OK) return st;
   if (!ctx->offloaded[i]) return fail(ctx, SPPO_ERR_STATE, "prefetch of chunk " + std::to_string(i) + " that was not offloaded");
   if (ctx->prefetched[i]) return fail(ctx, SPPO_ERR_STATE, "chunk " + std::to_string(i) + " already prefetched");
+  const int64_t r = ctx->rows[i];
+  if (r < chunk_len(ctx, i)) {
+    if (ctx->keep_ptr[i]) {
+      if (dst->keep != ctx->keep_ptr[i]) {
+        return fail(ctx, SPPO_ERR_INVALID_ARG, "dst.keep of chunk " + std::to_string(i) +
+                                                   " is not the keep buffer its offload filled");
+      }
+    } else {
+      bool same = dst->q == ctx->src_q[i] && dst->o == ctx->src_o[i] && dst->lse == ctx->src_lse[i];
+      for (size_t k = 0; same && k < ctx->extra_rb.size(); ++k) same = dst->extra[k] == ctx->src_extra[i][k];
+      if (!same) {
+        return fail(ctx, SPPO_ERR_STATE, "rows of chunk " + std::to_string(i) +
+                                             " past its offloaded prefix stayed in the offload's source buffers "
+                                             "(no keep buffer): the prefetch must target those buffers");
+      }
+    }
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (r < chunk_len(ctx, i) && ctx->keep_ptr[i]) {
+    SPPO_HIP(ctx, move_keep(ctx, i, r, dst->q, dst->o, dst->lse, dst->extra, ctx->keep_ptr[i], false, s));
+  }
   fold(ctx->t_h2d[i], ctx->ms_h2d);
   SPPO_HIP(ctx, hipEventRecord(ctx->ev_call[i], s));
   SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_call[i], 0));
   SPPO_HIP(ctx, hipStreamWaitEvent(ctx->h2d, ctx->ev_off[i], 0));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d[i].start, ctx->h2d));
   uint64_t bytes = 0;
-  SPPO_HIP(ctx, move_qol(ctx, i, ctx->rows[i], dst->q, dst->o, dst->lse, dst->extra, false, ctx->h2d, &bytes));
+  SPPO_HIP(ctx, move_qol(ctx, i, r, dst->q, dst->o, dst->lse, dst->extra, false, ctx->h2d, &bytes));
   SPPO_HIP(ctx, hipEventRecord(ctx->t_h2d[i].stop, ctx->h2d));
   SPPO_HIP(ctx, hipEventRecord(ctx->ev_pf[i], ctx->h2d));
   ctx->t_h2d[i].pending = true;
@@ -708,12 +802,53 @@ sppo_status sppo_get_offload_rows(const sppo_ctx* ctx, int64_t* out, int32_t cap
 
 sppo_status sppo_reset(sppo_ctx* ctx) {
   if (!ctx) return SPPO_ERR_INVALID_ARG;
+  // Copies of the abandoned walk may still read or write device buffers
+  // that the next walk reuses (and host slots that its offloads refill):
+  // wait for both copy streams (each also waits for the caller-stream
+  // events its copies were ordered behind) before forgetting them.
+  SPPO_HIP(ctx, hipStreamSynchronize(ctx->d2h));
+  SPPO_HIP(ctx, hipStreamSynchronize(ctx->h2d));
   ctx->in_bwd = false;
   ctx->next_fwd = 0;
   ctx->next_bwd = -1;
   std::fill(ctx->offloaded.begin(), ctx->offloaded.end(), 0);
   std::fill(ctx->prefetched.begin(), ctx->prefetched.end(), 0);
   std::fill(ctx->kv_prefetched.begin(), ctx->kv_prefetched.end(), 0);
+  std::fill(ctx->bwd_done.begin(), ctx->bwd_done.end(), 0);
+  return SPPO_OK;
+}
+
+size_t sppo_keep_bytes(const sppo_ctx* ctx, int32_t i) {
+  if (!ctx || i < 0 || i >= ctx->prob.n_chunks) return 0;
+  return keep_bytes(ctx, i);
+}
+
+sppo_status sppo_attn_finalize_chunk(sppo_ctx* ctx, int32_t i, const float* dk_acc, const float* dv_acc,
+                                     void* dk_out, void* dv_out, void* stream) {
+  sppo_status st = check_ctx_index(ctx, i);
+  if (st != SPPO_OK) return st;
+  if ((st = check_ptr(ctx, dk_acc, "dk_acc")) || (st = check_ptr(ctx, dv_acc, "dv_acc")) ||
+      (st = check_ptr(ctx, dk_out, "dk_out")) || (st = check_ptr(ctx, dv_out, "dv_out"))) {
+    return st;
+  }
+  if (dk_out == dv_out) return fail(ctx, SPPO_ERR_INVALID_ARG, "dk_out and dv_out must be distinct buffers");
+  if (!ctx->bwd_done[i]) {
+    return fail(ctx, SPPO_ERR_STATE, "finalize of chunk " + std::to_string(i) +
+                                         " before its backward in this walk");
+  }
+  sppo::FinalizeArgs a{};
+  a.dk = dk_acc;
+  a.dv = dv_acc;
+  a.out_k = dk_out;
+  a.out_v = dv_out;
+  a.B = ctx->prob.batch;
+  a.S = ctx->prob.seq_len;
+  a.W = (int64_t)ctx->prob.n_kv_heads * ctx->prob.head_dim;
+  a.row0 = ctx->off[i];
+  a.rows = chunk_len(ctx, i);
+  a.bf16 = ctx->prob.dtype == SPPO_BF16;
+  hipError_t e = sppo::launch_finalize(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(ctx, e, "finalize kernel launch");
   return SPPO_OK;
 }
 

@@ -41,6 +41,20 @@ hipError_t launch_bwd_pre_f32(const ChunkArgs& a, hipStream_t stream);
 hipError_t launch_bwd_dkdv_f32(const ChunkArgs& a, hipStream_t stream);
 hipError_t launch_bwd_dq_f32(const ChunkArgs& a, hipStream_t stream);
 
+// Rounding of finished dK/dV rows: out_k/out_v rows [row0, row0 + rows) of
+// every batch entry = dk/dv rows (fp32 [B, S, W], W = Hkv * D, W % 8 == 0),
+// as bf16 (round to nearest even) when bf16 != 0, else copied as fp32.
+// out_k/out_v have the accumulators' [B, S, W] layout; 16-byte aligned.
+struct FinalizeArgs {
+  const float* dk;
+  const float* dv;
+  void* out_k;
+  void* out_v;
+  int64_t B, S, W, row0, rows;
+  int bf16;
+};
+hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t stream);
+
 // Dense bf16 GEMM (fp32 accumulation), C[M, N] (op)= sum_k A(m, k) B(k, n).
 //   tn = 0 (NT): a is [M, K] (row stride lda), b is [N, K] (ldb); K % 64 == 0.
 //   tn = 1 (TN): a is stored [K, M], b is stored [K, N]; M % 256 == 0 and

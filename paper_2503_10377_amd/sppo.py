@@ -62,6 +62,7 @@ class sppo_chunk_bufs(ctypes.Structure):
         ("k", ctypes.c_void_p),
         ("v", ctypes.c_void_p),
         ("extra", ctypes.POINTER(ctypes.c_void_p)),
+        ("keep", ctypes.c_void_p),
     ]
 
 
@@ -141,6 +142,8 @@ def lib() -> ctypes.CDLL:
             "sppo_transpose_bf16": ([VP, VP, ctypes.c_int64, ctypes.c_int64, VP], ctypes.c_int),
             "sppo_pack_qkv_grad": ([ctypes.c_int64, I32, I32, VP, VP, VP, ctypes.c_int64, VP, VP], ctypes.c_int),
             "sppo_status_string": ([ctypes.c_int], ctypes.c_char_p),
+            "sppo_keep_bytes": ([P, I32], ctypes.c_size_t),
+            "sppo_attn_finalize_chunk": ([P, I32, VP, VP, VP, VP, VP], ctypes.c_int),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -154,7 +157,7 @@ def header_functions(path: str = HEADER_PATH) -> list[str]:
     """Names of the entry points declared in include/sppo.h."""
     with open(path) as f:
         text = f.read()
-    return re.findall(r"^(?:sppo_status|const char\*)\s+(sppo_\w+)\s*\(", text, flags=re.M)
+    return re.findall(r"^(?:sppo_status|const char\*|size_t)\s+(sppo_\w+)\s*\(", text, flags=re.M)
 
 
 def status_name(status: int) -> str:
@@ -257,8 +260,8 @@ def sppo_attn_bwd_chunk(ctx, i, q_i, k, v, o_i, lse_i, do_i, dq_i, dk_acc, dv_ac
                                           _ptr(dv_acc), _stream(stream)))
 
 
-def chunk_bufs(q=None, o=None, lse=None, k=None, v=None, extra=()) -> sppo_chunk_bufs:
-    b = sppo_chunk_bufs(_ptr(q), _ptr(o), _ptr(lse), _ptr(k), _ptr(v), None)
+def chunk_bufs(q=None, o=None, lse=None, k=None, v=None, extra=(), keep=None) -> sppo_chunk_bufs:
+    b = sppo_chunk_bufs(_ptr(q), _ptr(o), _ptr(lse), _ptr(k), _ptr(v), None, _ptr(keep))
     if len(extra):
         arr = (ctypes.c_void_p * len(extra))(*[_ptr(x) for x in extra])
         b.extra = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
@@ -280,6 +283,15 @@ def sppo_prefetch(ctx, i, dst: sppo_chunk_bufs, stream=None):
 
 def sppo_prefetch_kv(ctx, i, k, v, stream=None):
     _check(ctx, lib().sppo_prefetch_kv(_handle(ctx), i, _ptr(k), _ptr(v), _stream(stream)))
+
+
+def sppo_keep_bytes(ctx, i) -> int:
+    return int(lib().sppo_keep_bytes(_handle(ctx), i))
+
+
+def sppo_attn_finalize_chunk(ctx, i, dk_acc, dv_acc, dk_out, dv_out, stream=None):
+    _check(ctx, lib().sppo_attn_finalize_chunk(_handle(ctx), i, _ptr(dk_acc), _ptr(dv_acc), _ptr(dk_out),
+                                               _ptr(dv_out), _stream(stream)))
 
 
 def sppo_reset(ctx):

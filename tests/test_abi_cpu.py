@@ -26,7 +26,8 @@ def test_struct_layouts_match_c():
     # int64, int64, int32(+pad), ptr, int32 x3, enum, float, enum, int32(+pad), ptr
     assert ctypes.sizeof(L.sppo_problem) == 72
     assert L.sppo_problem.extra_row_bytes.offset == 64
-    assert ctypes.sizeof(L.sppo_chunk_bufs) == 48
+    assert ctypes.sizeof(L.sppo_chunk_bufs) == 56
+    assert L.sppo_chunk_bufs.keep.offset == 48
     assert ctypes.sizeof(L.sppo_copy_stats_t) == 40
     assert ctypes.sizeof(L.sppo_link_rates_t) == 24
 

@@ -7,6 +7,12 @@ size:
   * sampled query rows (O, LSE, dQ) at every chunk boundary, around the
     first tile edges, mid-chunk, and at random, for whole KV-head groups;
   * dK/dV of the last keys of the sequence (they only see the last rows);
+  * dK/dV of earlier keys, which accumulate over several backward calls of
+    the reverse walk: at 128K tokens, random keys of every chunk but the
+    last for two heads (every row of those heads enters the oracle); at
+    512K and 1M tokens, keys of the last 512 rows of chunk N-2 (rows from
+    there to the end: each such key accumulates over bwd(N-1) and bwd(N-2)),
+    the cost of an early key growing with the rows after it;
   * for 32K tokens, two complete heads against the full oracle;
   * invariants of the exact gradient over the whole tensors, in fp64 on the
     device: sum_j dK_j = 0, sum_j dV_j = sum_r dO_r (per KV group),
@@ -14,11 +20,14 @@ size:
 """
 import concurrent.futures as cf
 import math
+import os
 import sys
+import time
 
 import numpy as np
 import pytest
 import torch
+from threadpoolctl import threadpool_limits
 
 import oracle
 from paper_2503_10377_amd.chunked import ChunkedAttention
@@ -55,20 +64,29 @@ def host_group(t, g):
     return t[:, :, g:g + 1].float().cpu().numpy()
 
 
-def run_full(S, N, Hq, Hkv, D, offload, seed=0):
-    announce(f"full size S={S} N={N} Hq={Hq} Hkv={Hkv} D={D} offload={offload}: inputs")
+def run_full(S, N, Hq, Hkv, D, offload, seed=0, poison=False):
+    """The walk the benchmark times (two-chunk prefetch lookahead, every chunk
+    but the last offloaded).  With ``poison`` every device buffer an offload
+    makes dead -- the chunk's arena region, its rows of q and, when K/V are
+    evicted, the cache rows -- is overwritten with NaN once its copy has
+    landed, so any read of a buffer that was not brought back shows up.  The
+    inputs are generated again afterwards for the oracle side."""
+    announce(f"full size S={S} N={N} Hq={Hq} Hkv={Hkv} D={D} offload={offload} poison={poison}: inputs")
     inp = make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=seed, device="cuda")
     ca = ChunkedAttention(1, S, N, Hq, Hkv, D, dtype="bf16", offload=offload)
     out = ca.alloc_outputs()
     announce("HIP path: forward + backward walk")
-    ca.step(inp, out, lookahead=2)
+    ca.step(inp, out, lookahead=2, poison=poison)
     torch.cuda.synchronize()
-    announce("HIP path done")
+    announce(f"HIP path done (device arena {ca.arena.nbytes / 2**30:.2f} GiB)")
     res = {"o": out["o"], "lse": ca.lse_full(out), "dq": out["dq"], "dk": out["dk"], "dv": out["dv"]}
     for n, t in res.items():
         assert torch.isfinite(t).all(), n
     offsets = ca.offsets
     ca.close()
+    if poison:
+        del inp
+        inp = make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=seed, device="cuda")
     return inp, res, offsets
 
 
@@ -114,6 +132,45 @@ def check_tail_keys(inp, res, groups, T, S, Hq, Hkv, D):
         for g, dk, dv in ex.map(one, groups):
             check(f"dk_tail[g{g}]", res["dk"][:, t0:, g:g + 1].double().cpu().numpy(), dk, "bf16")
             check(f"dv_tail[g{g}]", res["dv"][:, t0:, g:g + 1].double().cpu().numpy(), dv, "bf16")
+
+
+def check_keys(inp, res, groups, keys, S, Hq, Hkv, D, rows_per_task=1024, row_block=128):
+    """dK/dV at ``keys`` for the KV groups ``groups`` against the oracle,
+    element by element: every row from the first key to the end of the
+    sequence, split into tasks over a thread pool (one BLAS thread each)
+    whose contributions are summed (oracle.keys_bwd_rows)."""
+    G = Hq // Hkv
+    scale = 1 / math.sqrt(D)
+    keys = np.array(sorted(set(int(x) for x in keys)))
+    lo = int(keys.min())
+    kv = {g: (host_group(inp["k"], g).astype(np.float64), host_group(inp["v"], g).astype(np.float64))
+          for g in groups}
+    tasks = [(g, r0, min(S, r0 + rows_per_task)) for g in groups for r0 in range(lo, S, rows_per_task)]
+    workers = max(1, min(16, len(os.sched_getaffinity(0))))
+    announce(f"oracle: {len(keys)} keys from row {lo} x groups {list(groups)}: {len(tasks)} tasks on {workers} threads")
+
+    def one(t):
+        g, r0, r1 = t
+        heads = list(range(g * G, (g + 1) * G))
+        rows = np.arange(r0, r1)
+        dk, dv = oracle.keys_bwd_rows(host_rows(inp["q"], rows, heads), host_rows(inp["do"], rows, heads), r0,
+                                      kv[g][0], kv[g][1], scale, keys, row_block=row_block)
+        return g, dk, dv
+
+    acc = {g: [0.0, 0.0] for g in groups}
+    t0, last = time.time(), time.time()
+    with threadpool_limits(1), cf.ThreadPoolExecutor(workers) as ex:
+        for n, (g, dk, dv) in enumerate(ex.map(one, tasks)):
+            acc[g][0] = acc[g][0] + dk
+            acc[g][1] = acc[g][1] + dv
+            if time.time() - last > 20:
+                last = time.time()
+                announce(f"  {n + 1}/{len(tasks)} tasks, {last - t0:.0f} s")
+    idx = torch.as_tensor(keys, device="cuda")
+    for g in groups:
+        check(f"dk_keys[g{g}]", res["dk"][:, idx, g:g + 1].double().cpu().numpy(), acc[g][0], "bf16")
+        check(f"dv_keys[g{g}]", res["dv"][:, idx, g:g + 1].double().cpu().numpy(), acc[g][1], "bf16")
+    announce(f"  keys checked in {time.time() - t0:.0f} s")
 
 
 def check_invariants(inp, res, Hq, Hkv, block=65536):
@@ -175,11 +232,15 @@ def test_seq128k_16chunks_offload():
     """bf16, 32 heads x 128, seq 131072 in 16 chunks of 8192, Q/K/V/O/LSE
     offloaded after each forward and prefetched before each backward."""
     S, N, Hq, Hkv, D = 131072, 16, 32, 32, 128
-    inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=0)
+    inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=0, poison=True)
     rng = np.random.default_rng(2)
     check_sampled_rows(inp, res, off, (0, Hkv - 1), sample_rows(off, S, 32, rng), Hq, Hkv, D)
     check_sampled_rows(inp, res, off, range(Hkv), sample_rows(off[-2:], S, 4, rng), Hq, Hkv, D)
     check_tail_keys(inp, res, (0, Hkv - 1), 512, S, Hq, Hkv, D)
+    # early keys: chunk boundaries and random keys of chunks 0..N-2
+    early = [0, 1, 127, 128, off[1] - 1, off[1], off[N // 2], off[N - 1] - 1]
+    early += rng.integers(0, off[N - 1], 56).tolist()
+    check_keys(inp, res, (0, Hkv - 1), early, S, Hq, Hkv, D)
     check_invariants(inp, res, Hq, Hkv)
 
 
@@ -188,22 +249,35 @@ def test_seq512k_32chunks_gqa_offload():
     """bf16 GQA, 32 query / 8 KV heads x 128, seq 524288 in 32 chunks of
     16384, per-chunk offload/prefetch."""
     S, N, Hq, Hkv, D = 524288, 32, 32, 8, 128
-    inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=0)
+    inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=0, poison=True)
     rng = np.random.default_rng(3)
     check_sampled_rows(inp, res, off, (0, Hkv - 1), sample_rows(off, S, 16, rng, every=4), Hq, Hkv, D)
     check_sampled_rows(inp, res, off, range(Hkv), np.array(sorted(rng.integers(0, S, 4))), Hq, Hkv, D)
     check_tail_keys(inp, res, (0, Hkv - 1), 256, S, Hq, Hkv, D)
+    c = off[N - 1]  # keys at the end of chunk N-2, accumulated over bwd(N-1) and bwd(N-2)
+    check_keys(inp, res, (0,), [c - 512, c - 129, c - 128, c - 1] + rng.integers(c - 512, c, 28).tolist(),
+               S, Hq, Hkv, D, row_block=64)
     check_invariants(inp, res, Hq, Hkv)
 
 
 @pytest.mark.timeout(1800)
 def test_seq1m_64chunks_offload():
     """bf16, 32 heads x 128, seq 1048576 in 64 chunks of 16384 (one GPU's
-    share of a multi-million-token sequence), full offload/prefetch walk."""
+    share of a multi-million-token sequence), full offload/prefetch walk
+    with poisoned dead buffers.  The same walk with the K/V cache evicted
+    after the forward walk (and poisoned) must give the same bits."""
     S, N, Hq, Hkv, D = 1048576, 64, 32, 32, 128
-    inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=0)
+    _, ev, _ = run_full(S, N, Hq, Hkv, D, "qkvol_evict", seed=0, poison=True)
+    inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=0, poison=True)
+    announce("evicting walk == resident walk, bitwise")
+    for n in res:
+        assert torch.equal(res[n], ev[n]), n
+    del ev
     rng = np.random.default_rng(4)
     check_sampled_rows(inp, res, off, (0, Hkv - 1), sample_rows(off, S, 16, rng, every=8), Hq, Hkv, D)
     check_sampled_rows(inp, res, off, range(0, Hkv, 4), np.array(sorted(rng.integers(0, S, 2))), Hq, Hkv, D)
     check_tail_keys(inp, res, (0, Hkv - 1), 128, S, Hq, Hkv, D)
+    c = off[N - 1]  # keys at the end of chunk N-2, accumulated over bwd(N-1) and bwd(N-2)
+    check_keys(inp, res, (0,), [c - 512, c - 129, c - 128, c - 1] + rng.integers(c - 512, c, 28).tolist(),
+               S, Hq, Hkv, D, row_block=64)
     check_invariants(inp, res, Hq, Hkv)

@@ -296,3 +296,82 @@ def test_offload_on_context_without_offload_is_rejected():
     assert ei.value.status == L.SPPO_ERR_STATE
     torch.cuda.synchronize()
     ca.close()
+
+
+def test_arena_frees_offloaded_chunks():
+    """Device staging arena (Sec. 5.2: an offloaded chunk's device memory is
+    given back once its copy has landed).  With every chunk but the last
+    offloaded, the walk holds its saved activations in an arena of 4 chunks
+    instead of all 16, gives the bits of the walk without offload,
+    and torch's peak of allocated device memory over a walk drops by the
+    difference; a second walk allocates nothing."""
+    B, S, Hq, Hkv, D = 1, 8192, 8, 2, 128
+    n = 16
+    res, peak, arena = {}, {}, {}
+    for mode in ("none", "qkvol"):
+        announce(f"arena memory, offload={mode}")
+        inp = make_inputs(B, S, Hq, Hkv, D, torch.bfloat16, seed=21, device="cuda")
+        ca = ChunkedAttention(B, S, n, Hq, Hkv, D, dtype="bf16", offload=mode)
+        out = ca.alloc_outputs(export=False)
+        torch.cuda.synchronize()
+        base = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        ca.step(inp, out, poison=(mode != "none"))
+        torch.cuda.synchronize()
+        peak[mode] = torch.cuda.max_memory_allocated() - base
+        arena[mode] = ca.arena.nbytes
+        region = ca._planes[0][1]
+        inp = make_inputs(B, S, Hq, Hkv, D, torch.bfloat16, seed=21, device="cuda")
+        torch.cuda.synchronize()
+        base = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        ca.step(inp, out)
+        torch.cuda.synchronize()
+        assert torch.cuda.max_memory_allocated() - base <= 1 << 20, "a walk allocated device memory"
+        res[mode] = {k: out[k].clone() for k in ("dq", "dk", "dv")}
+        ca.close()
+        del inp, out
+    for k in res["none"]:
+        assert torch.equal(res["none"][k], res["qkvol"][k]), k
+    assert arena["none"] == n * region and arena["qkvol"] == 4 * region
+    assert peak["none"] - peak["qkvol"] >= 0.9 * (arena["none"] - arena["qkvol"]), (peak, arena)
+
+
+def test_reset_orders_outstanding_copies():
+    """A walk abandoned with offloads and prefetches still in flight, then
+    reset: the next walk on the same context and buffers must give exactly
+    the bits of a clean run (reset waits for the abandoned copies)."""
+    S, Hq, Hkv, D, n = 4096, 4, 2, 128, 8
+    announce("reset with copies in flight")
+    inp = make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=13, device="cuda")
+    clean = ChunkedAttention(1, S, n, Hq, Hkv, D, dtype="bf16", offload="qkvol")
+    ref = clean.alloc_outputs()
+    clean.step(inp, ref)
+    torch.cuda.synchronize()
+    clean.close()
+    # The abandoned walk runs on other inputs, into the buffers the next walk
+    # fills, so a copy of it landing late would change the next walk's bits.
+    old = make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=99, device="cuda")
+    ca = ChunkedAttention(1, S, n, Hq, Hkv, D, dtype="bf16", offload="qkvol")
+    out = ca.alloc_outputs()
+    ctx, k, v = ca.ctx, old["k"], old["v"]
+    qc = [ca.chunk_view(old["q"], i) for i in range(n)]
+    oc = [ca.chunk_view(out["o"], i) for i in range(n)]
+    dc = [ca.chunk_view(old["do"], i) for i in range(n)]
+    dqc = [ca.chunk_view(out["dq"], i) for i in range(n)]
+    lse = out["lse"]
+    bufs = lambda i: L.chunk_bufs(q=qc[i], o=oc[i], lse=lse[i], k=k, v=v)  # noqa: E731
+    for i in range(n):
+        L.sppo_attn_fwd_chunk(ctx, i, qc[i], k, v, oc[i], lse[i])
+        L.sppo_offload_issue(ctx, i, bufs(i))
+    for i in (n - 1, n - 2, n - 3):
+        L.sppo_prefetch(ctx, i, bufs(i))
+    L.sppo_attn_bwd_chunk(ctx, n - 1, qc[n - 1], k, v, oc[n - 1], lse[n - 1], dc[n - 1], dqc[n - 1],
+                          out["dk"], out["dv"])
+    L.sppo_reset(ctx)  # no host synchronisation before it
+    ca.step(inp, out)
+    torch.cuda.synchronize()
+    for name in ("o", "dq", "dk", "dv"):
+        assert torch.equal(out[name], ref[name]), name
+    assert torch.equal(ca.lse_full(out), torch.cat(ref["lse"], dim=2))
+    ca.close()

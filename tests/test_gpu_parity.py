@@ -138,3 +138,34 @@ def test_chunked_matches_unchunked_on_gpu():
     for n in ("dk", "dv"):
         a, b = res[1][n].double(), res[4][n].double()
         assert ((a - b).norm() / a.norm()).item() < 1e-5, n
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_finalize_rounds_each_chunk_after_its_backward(dtype):
+    """Finalize: right after bwd(i), rows [c_i, c_{i+1}) of dK/dV are final
+    and are written in the problem's dtype -- bit for bit the fp32
+    accumulators rounded to nearest even (bf16) or copied (fp32) -- and
+    within the gates of the oracle.  Before its backward a chunk cannot be
+    finalized."""
+    B, S, Hq, Hkv, D = 2, 1000, 4, 2, 64
+    offsets = [0, 77, 300, 301, 1000]
+    announce(f"finalize {dtype}")
+    tdt = TORCH_DT[dtype]
+    inp = make_inputs(B, S, Hq, Hkv, D, tdt, seed=17, device="cuda")
+    host = {n: to_np(t) for n, t in inp.items()}
+    ca = ChunkedAttention(B, S, 4, Hq, Hkv, D, dtype=dtype, offsets=offsets, offload="qkvol")
+    out = ca.alloc_outputs()
+    fin = {n: torch.full((B, S, Hkv, D), float("nan"), dtype=tdt, device="cuda") for n in ("dk", "dv")}
+    with pytest.raises(L.SppoError) as ei:
+        L.sppo_attn_finalize_chunk(ca.ctx, 0, out["dk"], out["dv"], fin["dk"], fin["dv"])
+    assert ei.value.status == L.SPPO_ERR_STATE
+    ca.step(inp, out, finalize=fin)
+    torch.cuda.synchronize()
+    for n in ("dk", "dv"):
+        assert torch.equal(fin[n], out[n].to(tdt)), n
+    ref = oracle.attention(host["q"], host["k"], host["v"], host["do"], 1.0 / math.sqrt(D))
+    check_all({"dk": to_np(fin["dk"]), "dv": to_np(fin["dv"])}, ref, dtype, offsets)
+    with pytest.raises(L.SppoError) as ei:
+        L.sppo_attn_finalize_chunk(ca.ctx, 1, out["dk"], out["dv"], fin["dk"], fin["dk"])
+    assert ei.value.status == L.SPPO_ERR_INVALID_ARG
+    ca.close()

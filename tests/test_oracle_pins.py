@@ -246,6 +246,28 @@ def test_row_subset_and_tail_keys_match_full():
     np.testing.assert_allclose(dv, ref["dv"][:, t0:], atol=1e-13)
 
 
+def test_early_keys_from_row_blocks_match_full():
+    """keys_bwd_rows: the contributions of any partition of the rows
+    [min(keys), S) add up to the full oracle's dK/dV at those keys (early
+    keys included, GQA, repeated and unsorted keys), and rows before a key
+    contribute exactly nothing to it."""
+    B, S, Hq, Hkv, D = 2, 90, 4, 2, 8
+    q, k, v, do = rand_inputs(12, B, S, Hq, Hkv, D)
+    ref = oracle.attention(q, k, v, do, 0.3)
+    keys = np.array([40, 3, 89, 17, 40, 64, 65])
+    lo = int(keys.min())
+    dk = np.zeros((B, len(keys), Hkv, D))
+    dv = np.zeros_like(dk)
+    for r0, r1 in ((lo, 20), (20, 21), (21, 64), (64, S)):
+        a, b = oracle.keys_bwd_rows(q[:, r0:r1], do[:, r0:r1], r0, k, v, 0.3, keys, row_block=7)
+        dk += a
+        dv += b
+    np.testing.assert_allclose(dk, ref["dk"][:, keys], atol=1e-13)
+    np.testing.assert_allclose(dv, ref["dv"][:, keys], atol=1e-13)
+    a, b = oracle.keys_bwd_rows(q[:, :lo], do[:, :lo], 0, k, v, 0.3, keys)
+    assert not a.any() and not b.any()
+
+
 def _golden_value(x):
     if isinstance(x, list):
         return [_golden_value(y) for y in x]

@@ -327,11 +327,35 @@ sppo_status sppo_kernel_times(sppo_ctx* ctx, sppo_kernel_times_t* out, int32_t r
  * STATE if chunk i's prefetch was not issued. */
 sppo_status sppo_prefetch_wait(sppo_ctx* ctx, int32_t i, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * backward of one chunk [c0, c1) as sppo_attn_bwd_chunk enqueues it (same
+ * kernels, same results bit for bit), without a context and without any
+ * allocation.  Its Delta / LSE workspace is a static device array of the
+ * library (8 MiB on every GPU the library runs on, held until the process
+ * ends), so batch * n_q_heads * (c1 - c0) must not exceed 2^20
+ * (UNSUPPORTED otherwise).  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (several streams or threads) race, so the
+ * caller orders them (e.g. one stream).  Arguments as in sppo_create and
+ * sppo_attn_bwd_chunk: q_i, o_i, do_i, dq_i [B, c1 - c0, Hq, D] and lse_i
+ * [B, Hq, c1 - c0] chunk-local; k, v [B, S, Hkv, D]; dk_acc, dv_acc fp32
+ * [B, S, Hkv, D], rows [0, c1) overwritten (accumulate = 0) or added to
+ * (accumulate = 1), rows >= c1 untouched.  No call-order checks (there is
+ * no walk state).  Errors: INVALID_ARG, UNSUPPORTED, HIP, with the message
+ * in sppo_last_error(NULL) on the calling thread. */
+sppo_status sppo_attn_bwd_chunk_noalloc(int64_t batch, int64_t seq_len, int64_t c0, int64_t c1,
+                                        int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                        sppo_dtype dtype, float softmax_scale, int32_t accumulate,
+                                        const void* q_i, const void* k, const void* v, const void* o_i,
+                                        const float* lse_i, const void* do_i, void* dq_i, float* dk_acc,
+                                        float* dv_acc, void* stream);
+
 /* Chunk offsets as stored by the context (n_chunks + 1 values). */
 sppo_status sppo_get_offsets(const sppo_ctx* ctx, int64_t* out, int32_t capacity);
 
 /* Message for the last failure of this context ("" if none); with
- * ctx == NULL, the message of the last failed sppo_create on this thread. */
+ * ctx == NULL, the message of the last failed sppo_create or context-free
+ * attention call on this thread. */
 const char* sppo_last_error(const sppo_ctx* ctx);
 
 /* Static name of a status code. */

@@ -354,6 +354,10 @@ void destroy_all(sppo_ctx* c) {
 
 }  // namespace
 
+namespace sppo {
+void set_thread_error(const std::string& msg) { g_create_error = msg; }
+}  // namespace sppo
+
 extern "C" {
 
 const char* sppo_status_string(sppo_status s) {

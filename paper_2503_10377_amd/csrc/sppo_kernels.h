@@ -5,7 +5,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
 namespace sppo {
+
+// Message returned by sppo_last_error(NULL) on this thread: the failure of
+// the last context-free call (or of sppo_create).
+void set_thread_error(const std::string& msg);
 
 // Arguments of one chunk's attention kernels.  Chunk-local tensors (q, o,
 // dout, dq, lse) hold rows [c0, c1) only; k/v/dk/dv are full-length.

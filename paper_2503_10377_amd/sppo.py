@@ -143,6 +143,9 @@ def lib() -> ctypes.CDLL:
             "sppo_pack_qkv_grad": ([ctypes.c_int64, I32, I32, VP, VP, VP, ctypes.c_int64, VP, VP], ctypes.c_int),
             "sppo_status_string": ([ctypes.c_int], ctypes.c_char_p),
             "sppo_keep_bytes": ([P, I32], ctypes.c_size_t),
+            "sppo_attn_bwd_chunk_noalloc": ([ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, I32,
+                                             I32, I32, ctypes.c_int, ctypes.c_float, I32, VP, VP, VP, VP, VP, VP,
+                                             VP, VP, VP, VP], ctypes.c_int),
             "sppo_attn_finalize_chunk": ([P, I32, VP, VP, VP, VP, VP], ctypes.c_int),
         }
         for name, (args, res) in sig.items():
@@ -283,6 +286,17 @@ def sppo_prefetch(ctx, i, dst: sppo_chunk_bufs, stream=None):
 
 def sppo_prefetch_kv(ctx, i, k, v, stream=None):
     _check(ctx, lib().sppo_prefetch_kv(_handle(ctx), i, _ptr(k), _ptr(v), _stream(stream)))
+
+
+def sppo_attn_bwd_chunk_noalloc(batch, seq_len, c0, c1, n_q_heads, n_kv_heads, head_dim, dtype, softmax_scale,
+                                accumulate, q_i, k, v, o_i, lse_i, do_i, dq_i, dk_acc, dv_acc, stream=None):
+    dt = {"bf16": SPPO_BF16, "f32": SPPO_F32, "fp32": SPPO_F32}.get(dtype, dtype)
+    st = lib().sppo_attn_bwd_chunk_noalloc(batch, seq_len, c0, c1, n_q_heads, n_kv_heads, head_dim, dt,
+                                           softmax_scale, int(accumulate), _ptr(q_i), _ptr(k), _ptr(v), _ptr(o_i),
+                                           _ptr(lse_i), _ptr(do_i), _ptr(dq_i), _ptr(dk_acc), _ptr(dv_acc),
+                                           _stream(stream))
+    if st != SPPO_OK:
+        raise SppoError(st, lib().sppo_last_error(None).decode())
 
 
 def sppo_keep_bytes(ctx, i) -> int:

@@ -109,3 +109,28 @@ def test_layer_ops_reject_invalid_arguments_before_launch():
     assert lib.sppo_gelu_bf16(a, a, 12, None) == bad
     assert lib.sppo_transpose_bf16(a, a, 4, 4, None) == bad          # in place
     assert lib.sppo_pack_qkv_grad(4, 12, 8, a, a, a, 0, a, None) == bad  # wq % 8
+
+
+@pytest.mark.parametrize("change,status", [
+    (dict(S=65536, c1=65536, Hq=32), L.SPPO_ERR_UNSUPPORTED),  # B * Hq * (c1 - c0) > 2^20 workspace rows
+    (dict(D=96), L.SPPO_ERR_UNSUPPORTED),
+    (dict(c0=10, c1=10), L.SPPO_ERR_INVALID_ARG),
+    (dict(c1=5000), L.SPPO_ERR_INVALID_ARG),             # past seq_len
+    (dict(Hkv=3), L.SPPO_ERR_INVALID_ARG),
+    (dict(acc=2), L.SPPO_ERR_INVALID_ARG),
+    (dict(align=8), L.SPPO_ERR_INVALID_ARG),
+    (dict(same_dkdv=True), L.SPPO_ERR_INVALID_ARG),
+])
+def test_noalloc_backward_checks_arguments_on_the_host(change, status):
+    """The allocation-free backward validates everything before any HIP call
+    (so these run without a GPU)."""
+    a = dict(B=1, S=4096, c0=0, c1=1024, Hq=4, Hkv=2, D=128, acc=0, align=16, same_dkdv=False)
+    a.update(change)
+    p = [(1 << 20) + 16 * n if a["align"] == 16 else (1 << 20) + 8 for n in range(9)]
+    if a["same_dkdv"]:
+        p[8] = p[7]
+    with pytest.raises(L.SppoError) as ei:
+        L.sppo_attn_bwd_chunk_noalloc(a["B"], a["S"], a["c0"], a["c1"], a["Hq"], a["Hkv"], a["D"], "bf16", 0.0,
+                                      a["acc"], *p, stream=0)
+    assert ei.value.status == status
+    assert L.sppo_last_error(None)

@@ -160,6 +160,22 @@ def measured_traffic(kernel, workload):
     return rec.get("bytes_per_launch")
 
 
+def walk_memory(run_step, walk):
+    """Device memory a chunk walk needs (see device_memory in main)."""
+    import torch
+
+    torch.cuda.synchronize()
+    walk.arena = walk.keep = walk._layout = None
+    base = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+    run_step()
+    torch.cuda.synchronize()
+    return {"walk_peak_GiB": (torch.cuda.max_memory_allocated() - base) / 2**30,
+            "saved_activation_GiB": (walk.arena.nbytes + walk.keep.nbytes) / 2**30,
+            "arena_GiB": walk.arena.nbytes / 2**30, "keep_GiB": walk.keep.nbytes / 2**30,
+            "arena_high_water_GiB": walk.arena.high_water / 2**30}
+
+
 def copy_calibration(nbytes):
     """A plain device-to-device copy of ``nbytes``, three times: the known
     traffic against which FETCH_SIZE / WRITE_SIZE are scaled."""
@@ -337,6 +353,10 @@ def layer_bench(args):
                "d2h_GBps": cs["bytes_d2h"] / max(cs["ms_d2h"], 1e-9) / 1e6,
                "h2d_GBps": cs["bytes_h2d"] / max(cs["ms_h2d"], 1e-9) / 1e6}
         if lay_off is not None:
+            mem_on = walk_memory(lambda: lay.step(inp, p, out, lookahead=args.lookahead), lay)
+            mem_off = walk_memory(lambda: lay_off.step(inp, p, out, lookahead=args.lookahead), lay_off)
+            off["device_memory"] = {"offload": mem_on, "no_offload": mem_off,
+                                    "saved_GiB": mem_off["walk_peak_GiB"] - mem_on["walk_peak_GiB"]}
             per_off = sorted(times[1])
             ms_off = sum(per_off) / len(per_off)
             _, ph_off = breakdown(lay_off)
@@ -446,18 +466,13 @@ def main():
         return [span[("fwd", i)] for i in range(c.N)]
 
     def device_memory(c, o):
-        """Measured device memory of one walk: torch's peak of allocated
-        bytes over a step (inputs, outputs and the walk's buffers), and the
-        bytes the walk holds for the chunks' saved activations (its device
-        arena and keep buffers, allocated before the walk)."""
-        torch.cuda.synchronize()
-        torch.cuda.reset_peak_memory_stats()
-        c.step(inp, o, lookahead=args.lookahead)
-        torch.cuda.synchronize()
-        return {"peak_allocated_GiB": torch.cuda.max_memory_allocated() / 2**30,
-                "saved_activation_GiB": (c.arena.nbytes + c.keep.nbytes) / 2**30,
-                "arena_GiB": c.arena.nbytes / 2**30, "keep_GiB": c.keep.nbytes / 2**30,
-                "arena_high_water_GiB": c.arena.high_water / 2**30}
+        """Measured device memory of one walk: its buffers for the chunks'
+        saved activations are dropped, so the walk plans and allocates them
+        again inside one measured step; torch's peak of allocated bytes over
+        that step minus what was allocated before it is the walk's own
+        device memory (arena, keep buffers and anything else a step
+        allocates), independent of other walks alive in the process."""
+        return walk_memory(lambda: c.step(inp, o, lookahead=args.lookahead), c)
 
     def modelled_peak_bytes(t_fwd, lens, rows, copy_row, freed_row, bw_GBps):
         """Peak device bytes of the chunks' offloadable activations (Q, O,
@@ -586,8 +601,8 @@ def main():
             ca_off = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="none")
             ms_off, _, _ = timed(ca_off, steps, False)
             off["device_memory"] = {"offload": device_memory(ca, out), "no_offload": device_memory(ca_off, out)}
-            off["device_memory"]["saved_GiB"] = (off["device_memory"]["no_offload"]["peak_allocated_GiB"] -
-                                                 off["device_memory"]["offload"]["peak_allocated_GiB"])
+            off["device_memory"]["saved_GiB"] = (off["device_memory"]["no_offload"]["walk_peak_GiB"] -
+                                                 off["device_memory"]["offload"]["walk_peak_GiB"])
             # Per-chunk exposed time: one more step of each with an event at
             # every chunk boundary; exposed = duration with offload minus
             # duration without, per forward and per backward chunk.

@@ -12,7 +12,7 @@ import oracle
 from paper_2503_10377_amd import sppo as L
 from paper_2503_10377_amd.chunked import ChunkedAttention
 from paper_2503_10377_amd.inputs import make_inputs
-from parity import check_all, to_np
+from parity import check_all, check_structured, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -106,15 +106,12 @@ def test_bf16_structured(kind):
     that drops a row's own key (sharp_self) or admits the next key
     (sharp_future) moves O, LSE and dV by O(1), forward or backward.
 
-    These inputs make O and the gradients O(1-10) in magnitude, so the
-    max-abs gate is scaled by max(1, max|ref|) (a CPU emulation of the bf16
-    recipe -- bf16 O feeding Delta, bf16 P and dS feeding the MFMAs -- gives
-    max errors of 1-3e-2 here).  With sharp_self, P is one-hot and the true
-    dS, hence dQ and dK, is ~1e-7: those two tensors are pure cancellation
-    noise of dP - Delta and are not gated (a mask error there shows in dV)."""
+    The gates are parity.check_structured's, derived from the bf16 recipe
+    emulated on the CPU (tests/test_structured_gates_cpu.py): max-abs
+    scaled by max(1, max|ref|), and for sharp_self absolute gates only on
+    dQ and dK."""
     gpu, ref, off = run_case(1, 2048, 2, 1, 128, "bf16", N=4, seed=6, kind=kind)
-    check_all(gpu, ref, "bf16", off, skip=("dq", "dk") if kind == "sharp_self" else (),
-              scale_abs=True)
+    check_structured(gpu, ref, kind, off)
 
 
 def test_chunked_matches_unchunked_on_gpu():

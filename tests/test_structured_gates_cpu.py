@@ -1,0 +1,120 @@
+"""Where the bf16 gates for the structured inputs come from (CPU only).
+
+The stated bf16 tolerances were written for N(0,1) inputs.  The structured
+kinds (sharp_self: Q = 2K; sharp_future: Q_r = 2K_{r+1}; zero_q: Q = 0) give
+O(1-10) outputs and, for sharp_self, nearly one-hot P.  To see which gates a
+correct bf16 implementation can meet there, `bf16_recipe` applies to the
+exact computation the roundings of the precision reading -- P rounded to
+bf16 before the PV and dV products, O stored in bf16 and Delta formed from
+the stored O, dS rounded to bf16 before the dQ and dK products, dQ stored in
+bf16 -- and nothing else (fp64 otherwise).  It is test infrastructure: it
+shares nothing with the HIP path and says only what the rounding points
+cost.  The tests check, on the inputs and shapes of the GPU test:
+  * the recipe passes parity.check_structured (the gate accepts a correct
+    bf16 result, with margin);
+  * the recipe fails the gates that check_structured relaxes (each
+    relaxation is needed);
+  * results of a mask shifted by one key fail check_structured on the kind
+    built to expose that shift (sharp_self: a mask that hides a row's own
+    key; sharp_future: one that admits the next key), so the relaxed gates
+    still see the mistakes the structured inputs exist to catch."""
+import math
+import types
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import causal_attention as oracle_mod
+from paper_2503_10377_amd.inputs import make_inputs
+from parity import GateError, check, check_all, check_structured
+
+S, Hq, Hkv, D, N = 2048, 2, 1, 128, 4
+
+
+def bf16(x):
+    """Round to bf16 (nearest even) and back to fp64."""
+    return torch.from_numpy(np.ascontiguousarray(x)).float().to(torch.bfloat16).double().numpy()
+
+
+def bf16_recipe(q, k, v, do, scale):
+    B, S_, H, _ = q.shape
+    G = H // k.shape[2]
+    out = {"o": np.zeros_like(q), "lse": np.zeros((B, H, S_)), "dq": np.zeros_like(q),
+           "dk": np.zeros_like(k), "dv": np.zeros_like(v)}
+    hidden = np.arange(S_)[None, :] > np.arange(S_)[:, None]
+    for b in range(B):
+        for h in range(H):
+            g = h // G
+            qh, kh, vh, doh = q[b, :, h], k[b, :, g], v[b, :, g], do[b, :, h]
+            s = scale * (qh @ kh.T)
+            s[hidden] = -np.inf
+            m = s.max(axis=1, keepdims=True)
+            p = np.exp(s - m)
+            l_ = p.sum(axis=1, keepdims=True)
+            o = bf16((bf16(p) @ vh) / l_)
+            lse = (m + np.log(l_))[:, 0]
+            delta = (doh * o).sum(axis=1)
+            P = np.exp(s - lse[:, None])
+            dS = P * (doh @ vh.T - delta[:, None])
+            out["o"][b, :, h], out["lse"][b, h] = o, lse
+            out["dv"][b, :, g] += bf16(P).T @ doh
+            out["dq"][b, :, h] = bf16(scale * (bf16(dS) @ kh))
+            out["dk"][b, :, g] += scale * (bf16(dS).T @ qh)
+    return out
+
+
+@pytest.fixture(scope="module", params=["sharp_self", "sharp_future", "zero_q"])
+def case(request):
+    kind = request.param
+    inp = make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=6, device="cpu", kind=kind)
+    h = {n: t.double().numpy() for n, t in inp.items()}
+    scale = 1 / math.sqrt(D)
+    ref = oracle.attention(h["q"], h["k"], h["v"], h["do"], scale)
+    return kind, h, scale, ref, list(oracle.equal_offsets(S, N))
+
+
+def test_recipe_passes_the_structured_gates_with_margin(case):
+    kind, h, scale, ref, off = case
+    got = bf16_recipe(h["q"], h["k"], h["v"], h["do"], scale)
+    res = check_structured(got, ref, kind, off)
+    for n in ("o", "dq", "dk", "dv"):
+        bound = 2e-2 * max(1.0, float(np.abs(ref[n]).max()))
+        assert res[n]["max_abs"] <= 0.7 * bound, (n, res[n])
+
+
+def test_each_relaxation_is_needed(case):
+    kind, h, scale, ref, off = case
+    got = bf16_recipe(h["q"], h["k"], h["v"], h["do"], scale)
+    if kind == "sharp_future":
+        with pytest.raises(GateError):  # the unscaled max-abs gate on dK
+            check("dk", got["dk"], ref["dk"], "bf16", offsets=off)
+    elif kind == "sharp_self":
+        for n in ("dq", "dk"):
+            with pytest.raises(GateError):  # the per-chunk relative gate
+                check(n, got[n], ref[n], "bf16", offsets=off)
+    else:
+        check_all(got, ref, "bf16", off)  # zero_q needs no relaxation
+
+
+SHIFTS = {
+    "sharp_future": ("keys[None, :] > rows[:, None]", "keys[None, :] > rows[:, None] + 1"),  # admits key r+1
+    "sharp_self": ("keys[None, :] > rows[:, None]", "keys[None, :] > rows[:, None] - 1"),    # hides key r
+}
+
+
+def test_shifted_mask_fails_the_structured_gates(case):
+    kind, h, scale, ref, off = case
+    if kind not in SHIFTS:
+        pytest.skip("Q = 0 checks the uniform prefix mean, not the mask edge")
+    mutation = SHIFTS[kind]
+    with open(oracle_mod.__file__) as f:
+        src = f.read()
+    mod = types.ModuleType("oracle_mutant")
+    exec(compile(src.replace(*mutation), "oracle_mutant", "exec"), mod.__dict__)
+    with np.errstate(all="ignore"):
+        bad = mod.attention(h["q"], h["k"], h["v"], h["do"], scale)
+    bad = {n: np.nan_to_num(x, nan=0.0) for n, x in bad.items()}
+    with pytest.raises(GateError):
+        check_structured(bad, ref, kind, off)

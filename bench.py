@@ -436,6 +436,7 @@ def main():
         for _ in range(args.warmup):
             c.step(inp, o, lookahead=args.lookahead)
         torch.cuda.synchronize()
+        print(f"[bench] warmup done (offload {c.offload}, kernel events {bool(timing)})", file=sys.stderr, flush=True)
         L.sppo_copy_stats(c.ctx, reset_after=True)
         L.sppo_set_kernel_timing(c.ctx, timing)
         L.sppo_kernel_times(c.ctx, reset_after=True)
@@ -600,7 +601,12 @@ def main():
         if not args.no_offload_compare:
             ca_off = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="none")
             ms_off, _, _ = timed(ca_off, steps, False)
-            off["device_memory"] = {"offload": device_memory(ca, out), "no_offload": device_memory(ca_off, out)}
+            print(f"[bench] no offload: ms/step={ms_off:.2f}", file=sys.stderr, flush=True)
+            mem_on = device_memory(ca, out)
+            print(f"[bench] device memory with offload: {mem_on['walk_peak_GiB']:.3f} GiB", file=sys.stderr, flush=True)
+            mem_off = device_memory(ca_off, out)
+            print(f"[bench] device memory without: {mem_off['walk_peak_GiB']:.3f} GiB", file=sys.stderr, flush=True)
+            off["device_memory"] = {"offload": mem_on, "no_offload": mem_off}
             off["device_memory"]["saved_GiB"] = (off["device_memory"]["no_offload"]["walk_peak_GiB"] -
                                                  off["device_memory"]["offload"]["walk_peak_GiB"])
             # Per-chunk exposed time: one more step of each with an event at
@@ -612,6 +618,7 @@ def main():
                 c.step(inp, out, lookahead=args.lookahead, marks=marks)
                 torch.cuda.synchronize()
                 spans[name] = {marks[n][0]: marks[n][1].elapsed_time(marks[n + 1][1]) for n in range(len(marks) - 1)}
+                print(f"[bench] marked step ({name})", file=sys.stderr, flush=True)
             off["per_chunk_exposed_ms"] = {
                 ph: [round(spans["on"][(ph, i)] - spans["off"][(ph, i)], 3) for i in range(N)] for ph in ("fwd", "bwd")}
             ca_off.close()
@@ -626,6 +633,7 @@ def main():
                 ca_q = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="qol")
                 ms_q, _, cs_q = timed(ca_q, steps, False)
                 ca_q.close()
+                print(f"[bench] Q/O/LSE-only offload: ms/step={ms_q:.2f}", file=sys.stderr, flush=True)
                 copy_q = (cs_q["ms_d2h"] + cs_q["ms_h2d"]) / steps
                 exp_q = max(0.0, ms_q - ms_off)
                 off["round_trip_qol"] = {
@@ -638,6 +646,7 @@ def main():
                 ca_ev = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="qkvol_evict")
                 ms_evict, _, cs_ev = timed(ca_ev, steps, False)
                 ca_ev.close()
+                print(f"[bench] K/V-evicting walk: ms/step={ms_evict:.2f}", file=sys.stderr, flush=True)
                 copy_ev = (cs_ev["ms_d2h"] + cs_ev["ms_h2d"]) / steps
                 exp_ev = max(0.0, ms_evict - ms_off)
                 off["evict"] = {

@@ -162,10 +162,13 @@ def measured_traffic(kernel, workload):
 
 def walk_memory(run_step, walk):
     """Device memory a chunk walk needs (see device_memory in main)."""
+    import gc
+
     import torch
 
     torch.cuda.synchronize()
     walk.arena = walk.keep = walk._layout = None
+    gc.collect()  # nothing else is freed inside the measured step
     base = torch.cuda.memory_allocated()
     torch.cuda.reset_peak_memory_stats()
     run_step()

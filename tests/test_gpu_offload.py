@@ -12,6 +12,7 @@
   stays bitwise equal to the run without offload.
 * Order/state violations return the documented status and enqueue nothing.
 """
+import gc
 import sys
 
 import pytest
@@ -313,6 +314,7 @@ def test_arena_frees_offloaded_chunks():
         inp = make_inputs(B, S, Hq, Hkv, D, torch.bfloat16, seed=21, device="cuda")
         ca = ChunkedAttention(B, S, n, Hq, Hkv, D, dtype="bf16", offload=mode)
         out = ca.alloc_outputs(export=False)
+        gc.collect()  # tensors of earlier tests freed now, not in the middle of the measured step
         torch.cuda.synchronize()
         base = torch.cuda.memory_allocated()
         torch.cuda.reset_peak_memory_stats()
@@ -322,6 +324,7 @@ def test_arena_frees_offloaded_chunks():
         arena[mode] = ca.arena.nbytes
         region = ca._planes[0][1]
         inp = make_inputs(B, S, Hq, Hkv, D, torch.bfloat16, seed=21, device="cuda")
+        gc.collect()
         torch.cuda.synchronize()
         base = torch.cuda.memory_allocated()
         torch.cuda.reset_peak_memory_stats()

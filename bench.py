@@ -13,10 +13,12 @@ Reported (one JSON line):
                  causal half only
   pct_peak       value / 2516.6 TFLOP/s (256 CU x 2.4 GHz x 4096 bf16
                  flop/clk/CU, dense)
-  offload_hidden 1 - max(0, T_on - T_off) / T_copy, where T_off is the same
-                 step without offload and T_copy the event-timed copy busy
-                 time per step; the same for the K/V-evicting walk under
-                 offload.evict
+  offload_hidden 1 - max(0, T_on - T_off) / T_copy, where T_on and T_off are
+                 the step with and without offload, timed in alternating
+                 steps (so drift over the run falls on both), and T_copy the
+                 event-timed copy busy time per step; the same for the
+                 Q/O/LSE-only walk (offload.round_trip_qol) and the
+                 K/V-evicting walk (offload.evict)
   ms_per_step_median / _min   over the K headline steps (an event between
                  steps)
   offload.per_chunk_exposed_ms   per forward / backward chunk, duration with
@@ -460,6 +462,37 @@ def main():
 
     step_times = []
 
+    def alternate(walks, steps, o=None):
+        """Time several walks in alternating steps: args.warmup steps of each,
+        then `steps` rounds of one event-timed step of each in turn.
+        Returns per walk the mean ms per step, the step times and the copy
+        statistics of the timed steps (None without offload)."""
+        o = out if o is None else o
+        for w in walks.values():
+            for _ in range(args.warmup):
+                w.step(inp, o, lookahead=args.lookahead)
+        torch.cuda.synchronize()
+        for w in walks.values():
+            if w.offload != L.SPPO_OFFLOAD_NONE:
+                L.sppo_copy_stats(w.ctx, reset_after=True)
+        st = torch.cuda.current_stream()
+        ev = {k: [] for k in walks}
+        for n in range(steps):
+            for k, w in walks.items():
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(st)
+                w.step(inp, o, lookahead=args.lookahead)
+                e1.record(st)
+                ev[k].append((e0, e1))
+            torch.cuda.synchronize()
+            print(f"[bench] alternating round {n + 1}/{steps} ({', '.join(walks)})", file=sys.stderr, flush=True)
+        res_ = {}
+        for k, w in walks.items():
+            t = [e0.elapsed_time(e1) for e0, e1 in ev[k]]
+            cs_ = L.sppo_copy_stats(w.ctx, reset_after=True) if w.offload != L.SPPO_OFFLOAD_NONE else None
+            res_[k] = {"ms": sum(t) / len(t), "steps": t, "cs": cs_}
+        return res_
+
     def chunk_fwd_ms(c, o):
         """Forward duration of each chunk, from one step with an event at
         every chunk boundary."""
@@ -505,38 +538,46 @@ def main():
         """Sequence-aware offloading (NEXT-1): equal vs FLOPs-balanced chunk
         boundaries, each with the full offload set and with the planned row
         prefix per chunk (copy of chunk i bounded by the forward of chunk
-        i+1 at the isolated link rate)."""
+        i+1 at the isolated link rate); the walks without offload, with the
+        full set and with the plan are timed in alternating steps."""
         result = {}
         freed_row = B * (2 * Hq * D * 2 + 4 * Hq)
         for part in ("equal", "balanced"):
             offs = None if part == "equal" else L.sppo_balanced_offsets(S, N, 128)
             c_none = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offsets=offs, offload="none")
             o = c_none.alloc_outputs(export=False)
-            ms_none, _, _ = timed(c_none, steps, False, o)
+            c_none.step(inp, o, lookahead=args.lookahead)
             t_fwd = chunk_fwd_ms(c_none, o)
-            mem_none = device_memory(c_none, o)
-            c_none.close()
-            c_on = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offsets=offs, offload="qkvol")
-            lens = [c_on.chunk_len(i) for i in range(N)]
-            copy_row = c_on.offload_bytes_per_row()
-            plan = L.sppo_plan_offload_rows(c_on.offsets, copy_row, bw_GBps, t_fwd[1:] + [0.0], 128)
-            entry = {"offsets": c_on.offsets, "ms_per_step_no_offload": ms_none, "fwd_ms_per_chunk": t_fwd,
-                     "device_memory_no_offload": mem_none}
-            for name, rows in (("full", lens[:-1] + [0]), ("plan", plan)):
-                c_on.set_offload_rows(rows)
-                ms, _, cs_p = timed(c_on, steps, False, o)
+            lens = [c_none.chunk_len(i) for i in range(N)]
+            walks = {"none": c_none}
+            for name in ("full", "plan"):
+                walks[name] = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offsets=offs, offload="qkvol")
+            copy_row = walks["full"].offload_bytes_per_row()
+            rows_of = {"full": lens[:-1] + [0],
+                       "plan": L.sppo_plan_offload_rows(c_none.offsets, copy_row, bw_GBps, t_fwd[1:] + [0.0], 128)}
+            for name in ("full", "plan"):
+                walks[name].set_offload_rows(rows_of[name])
+            alt = alternate(walks, steps, o)  # steps of the three walks in turn
+            ms_none = alt["none"]["ms"]
+            entry = {"offsets": c_none.offsets, "ms_per_step_no_offload": ms_none,
+                     "ms_steps_no_offload": [round(x, 2) for x in alt["none"]["steps"]], "fwd_ms_per_chunk": t_fwd,
+                     "device_memory_no_offload": device_memory(c_none, o)}
+            for name in ("full", "plan"):
+                rows, ms, cs_p = rows_of[name], alt[name]["ms"], alt[name]["cs"]
                 copy_p = (cs_p["ms_d2h"] + cs_p["ms_h2d"]) / steps
                 exp_p = max(0.0, ms - ms_none)
                 entry[name] = {
                     "rows": rows, "alpha": [round(r / n, 4) for r, n in zip(rows, lens)],
-                    "ms_per_step": ms, "tflops": flops["total"] / (ms * 1e-3) / 1e12,
+                    "ms_per_step": ms, "ms_steps": [round(x, 2) for x in alt[name]["steps"]],
+                    "tflops": flops["total"] / (ms * 1e-3) / 1e12,
                     "bytes_d2h_per_step": cs_p["bytes_d2h"] / steps, "copy_ms_per_step": copy_p,
                     "exposed_ms_per_step": exp_p,
                     "hidden_pct": 100.0 * max(0.0, min(1.0, 1.0 - exp_p / copy_p)) if copy_p > 0 else None,
                     "modelled_peak_activation_GiB": modelled_peak_bytes(
                         t_fwd, lens, rows, copy_row, freed_row, bw_GBps) / 2**30,
-                    "device_memory": device_memory(c_on, o)}
-            c_on.close()
+                    "device_memory": device_memory(walks[name], o)}
+            for w in walks.values():
+                w.close()
             result[part] = entry
             print(f"[bench] policy {part}: full {entry['full']['ms_per_step']:.1f} ms, "
                   f"plan {entry['plan']['ms_per_step']:.1f} ms", file=sys.stderr, flush=True)
@@ -602,9 +643,45 @@ def main():
                "h2d_GBps": cs["bytes_h2d"] / max(cs["ms_h2d"], 1e-9) / 1e6}
         off["kv_copy_only"] = offload == "qkvol"
         if not args.no_offload_compare:
+            # The headline walk, the walk that offloads only Q/O/LSE (the set
+            # that makes the round trip; in the headline walk K/V are also
+            # copied out but never needed back) and the walk that evicts the
+            # K/V cache after the forward and streams it back under the last
+            # chunk's backward, each timed in alternating steps with the walk
+            # without offload, so that clock drift over the run falls on both
+            # sides of each comparison alike.
             ca_off = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="none")
-            ms_off, _, _ = timed(ca_off, steps, False)
-            print(f"[bench] no offload: ms/step={ms_off:.2f}", file=sys.stderr, flush=True)
+            alt = {}
+
+            def hidden_of(name):
+                a, ms_none = alt[name], alt[name]["ms_none"]
+                copy = (a["cs"]["ms_d2h"] + a["cs"]["ms_h2d"]) / steps
+                exp = max(0.0, a["ms"] - ms_none)
+                return {"ms_per_step": a["ms"], "ms_per_step_no_offload": ms_none,
+                        "ms_steps": [round(x, 2) for x in a["steps"]],
+                        "ms_steps_no_offload": [round(x, 2) for x in a["steps_none"]],
+                        "bytes_d2h_per_step": a["cs"]["bytes_d2h"] / steps,
+                        "bytes_h2d_per_step": a["cs"]["bytes_h2d"] / steps, "copy_ms_per_step": copy,
+                        "exposed_ms_per_step": exp,
+                        "hidden_pct": 100.0 * max(0.0, min(1.0, 1.0 - exp / copy)) if copy > 0 else None}
+
+            # each offloading walk alternates with the walk without offload
+            for name in ("offload", "qol", "evict") if offload == "qkvol" else ("offload",):
+                w = ca if name == "offload" else ChunkedAttention(
+                    B, S, N, Hq, Hkv, D, dtype="bf16", offload={"qol": "qol", "evict": "qkvol_evict"}[name])
+                pair = alternate({name: w, "none": ca_off}, steps)
+                alt[name] = dict(pair[name], ms_none=pair["none"]["ms"], steps_none=pair["none"]["steps"])
+                if w is not ca:
+                    w.close()
+            head = hidden_of("offload")
+            ms_off = head["ms_per_step_no_offload"]
+            off["ms_per_step_no_offload"] = ms_off
+            off["ms_per_step_offload_alternating"] = head["ms_per_step"]
+            off["exposed_ms_per_step"] = head["exposed_ms_per_step"]
+            off["hidden_pct"] = head["hidden_pct"]
+            if offload == "qkvol":
+                off["round_trip_qol"] = hidden_of("qol")
+                off["evict"] = hidden_of("evict")
             mem_on = device_memory(ca, out)
             print(f"[bench] device memory with offload: {mem_on['walk_peak_GiB']:.3f} GiB", file=sys.stderr, flush=True)
             mem_off = device_memory(ca_off, out)
@@ -625,37 +702,6 @@ def main():
             off["per_chunk_exposed_ms"] = {
                 ph: [round(spans["on"][(ph, i)] - spans["off"][(ph, i)], 3) for i in range(N)] for ph in ("fwd", "bwd")}
             ca_off.close()
-            exposed = max(0.0, ms_on - ms_off)
-            off["ms_per_step_no_offload"] = ms_off
-            off["exposed_ms_per_step"] = exposed
-            off["hidden_pct"] = 100.0 * max(0.0, min(1.0, 1.0 - exposed / copy_ms)) if copy_ms > 0 else None
-            if offload == "qkvol":
-                # The round-trip set alone: Q/O/LSE go out and come back, K/V
-                # are not copied at all (in the headline walk they are copied
-                # to the host and never needed back).
-                ca_q = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="qol")
-                ms_q, _, cs_q = timed(ca_q, steps, False)
-                ca_q.close()
-                print(f"[bench] Q/O/LSE-only offload: ms/step={ms_q:.2f}", file=sys.stderr, flush=True)
-                copy_q = (cs_q["ms_d2h"] + cs_q["ms_h2d"]) / steps
-                exp_q = max(0.0, ms_q - ms_off)
-                off["round_trip_qol"] = {
-                    "ms_per_step": ms_q, "bytes_d2h_per_step": cs_q["bytes_d2h"] / steps,
-                    "bytes_h2d_per_step": cs_q["bytes_h2d"] / steps, "copy_ms_per_step": copy_q,
-                    "exposed_ms_per_step": exp_q,
-                    "hidden_pct": 100.0 * max(0.0, min(1.0, 1.0 - exp_q / copy_q)) if copy_q > 0 else None}
-                # The same walk with the K/V cache rows given up after the
-                # forward and streamed back under the last chunk's backward.
-                ca_ev = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype="bf16", offload="qkvol_evict")
-                ms_evict, _, cs_ev = timed(ca_ev, steps, False)
-                ca_ev.close()
-                print(f"[bench] K/V-evicting walk: ms/step={ms_evict:.2f}", file=sys.stderr, flush=True)
-                copy_ev = (cs_ev["ms_d2h"] + cs_ev["ms_h2d"]) / steps
-                exp_ev = max(0.0, ms_evict - ms_off)
-                off["evict"] = {
-                    "ms_per_step": ms_evict, "bytes_h2d_per_step": cs_ev["bytes_h2d"] / steps,
-                    "copy_ms_per_step": copy_ev, "exposed_ms_per_step": exp_ev,
-                    "hidden_pct": 100.0 * max(0.0, min(1.0, 1.0 - exp_ev / copy_ev)) if copy_ev > 0 else None}
         # Host-link rates of the library's copy path with nothing else
         # running (1 GiB each way, and both ways at once); T_copy_iso is the
         # step's copy volume at those rates.

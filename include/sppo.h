@@ -104,7 +104,8 @@ typedef struct {
                                     full layer's saved tensors, Sec. 5.1:
                                     everything but K/V is offloadable)      */
   const size_t* extra_row_bytes; /* host array of n_extra row sizes (bytes
-                                    per token, > 0); plane k of chunk i is a
+                                    per token, positive multiples of 4);
+                                    plane k of chunk i is a
                                     chunk-local [B, s_i, extra_row_bytes[k]]
                                     byte array; NULL when n_extra == 0      */
 } sppo_problem;
@@ -123,11 +124,11 @@ typedef struct {
                    < s_i, see sppo_set_offload_rows) the rows [rows_i, s_i)
                    of Q_i, O_i, LSE_i and the extra planes stay on the
                    device.  With a keep buffer, sppo_offload_issue moves
-                   them there (a device-to-device copy on its stream), so
+                   them there (a copy kernel on its stream), so
                    the source buffers are dead as a whole after
                    sppo_offload_wait and can be reused (a device staging
                    ring), and sppo_prefetch moves them back into its
-                   destination buffers (on its stream) -- pass the same
+                   destination buffers (a copy kernel on its stream) -- pass the same
                    keep pointer to both.  Without one, they stay in the
                    source buffers, and the prefetch must target those same
                    buffers.  Ignored when rows_i == s_i.  The caller owns
@@ -159,13 +160,18 @@ typedef struct {
 } sppo_kernel_times_t;
 
 /* Create a context: validates the problem, copies the offsets, allocates
- * the Delta workspace (fp32 [B, Hq, max s_i]) on the current device, two
- * copy streams (default priority) and per-chunk events, and -- unless
- * offload is NONE -- page-locked host slots for every chunk's offload set.
+ * the Delta workspace (fp32 [B, Hq, max s_i]) on the current device and
+ * per-chunk events, takes a reference on the device's two copy streams
+ * (device->host and host->device, default priority, created by the first
+ * context on the device and shared by all of its contexts, so the library
+ * adds two streams to a process however many contexts it has), and --
+ * unless offload is NONE -- allocates page-locked host slots for every
+ * chunk's offload set.
  * *out is set only on success.  Errors: INVALID_ARG, UNSUPPORTED, OOM, HIP. */
 sppo_status sppo_create(const sppo_problem* problem, sppo_ctx** out);
 
-/* Synchronise the context's copy streams and free everything it owns.
+/* Synchronise the copy streams and free everything the context owns (the
+ * copy streams go when the last context on the device is destroyed).
  * Safe on NULL. */
 sppo_status sppo_destroy(sppo_ctx* ctx);
 

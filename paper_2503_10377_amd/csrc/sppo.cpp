@@ -1,9 +1,17 @@
 // libsppo host side: the C ABI declared in include/sppo.h.
 //
 // Owns, per context: the chunk partition (offsets c_0..c_N), a backward
-// workspace on the device (Delta and LSE * log2 e), two non-blocking copy streams (device->host and
-// host->device, default priority), per-chunk events, and page-locked host
-// slots holding each chunk's offload set.  Kernels run on the caller's
+// workspace on the device (Delta and LSE * log2 e), per-chunk events, and
+// page-locked host slots holding each chunk's offload set.  The two
+// non-blocking copy streams (device->host and host->device, default
+// priority) are shared by every context on a device: each stream the process
+// creates takes a hardware queue, and with more streams than queues the
+// runtime puts several streams on one in-order queue, so a compute stream
+// sharing a queue with a copy stream waited for that stream's copies (about
+// 80 ms per 128K-token step was measured with four contexts alive).  One
+// pair per device keeps the library at two streams whatever the number of
+// contexts (one per layer of a model, say); copies of different contexts
+// then run one after another, as they would on the single host link anyway.  Kernels run on the caller's
 // stream; copies run on the context's streams and are ordered against the
 // caller's stream with events only, so nothing blocks the host.
 //
@@ -28,6 +36,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -109,6 +118,45 @@ sppo_status hip_fail(sppo_ctx* ctx, hipError_t e, const char* what) {
   } while (0)
 
 bool aligned16(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// The copy streams shared by the contexts of each device (reference counted;
+// the last context on a device destroys them).
+struct CopyStreams {
+  hipStream_t d2h = nullptr, h2d = nullptr;
+  int refs = 0;
+};
+constexpr int kMaxDevices = 64;
+CopyStreams g_copy[kMaxDevices];
+std::mutex g_copy_mu;
+
+hipError_t acquire_copy_streams(int dev, hipStream_t* d2h, hipStream_t* h2d) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_copy_mu);
+  CopyStreams& cs = g_copy[dev];
+  if (cs.refs == 0) {
+    hipError_t e = hipStreamCreateWithFlags(&cs.d2h, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&cs.h2d, hipStreamNonBlocking);
+    if (e != hipSuccess) {
+      if (cs.d2h) (void)hipStreamDestroy(cs.d2h);
+      cs.d2h = cs.h2d = nullptr;
+      return e;
+    }
+  }
+  cs.refs += 1;
+  *d2h = cs.d2h;
+  *h2d = cs.h2d;
+  return hipSuccess;
+}
+
+void release_copy_streams(int dev) {
+  std::lock_guard<std::mutex> lock(g_copy_mu);
+  CopyStreams& cs = g_copy[dev];
+  if (--cs.refs == 0) {
+    (void)hipStreamDestroy(cs.d2h);
+    (void)hipStreamDestroy(cs.h2d);
+    cs.d2h = cs.h2d = nullptr;
+  }
+}
 
 int64_t chunk_len(const sppo_ctx* c, int i) { return c->off[i + 1] - c->off[i]; }
 
@@ -276,14 +324,14 @@ hipError_t move_keep(sppo_ctx* c, int i, int64_t r, void* q, void* o, float* lse
   if (t == 0) return hipSuccess;
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t row = (size_t)c->prob.n_q_heads * c->prob.head_dim * c->elt;
-  const hipMemcpyKind kind = hipMemcpyDeviceToDevice;
   char* kp = static_cast<char*>(keep);
   hipError_t e = hipSuccess;
   // [B, s_i, w] plane: B spans of t*w bytes at row r, pitch s_i*w <-> t*w.
+  // Moved by a kernel on the caller's stream (sppo::launch_copy_rows).
   auto plane = [&](void* dev, size_t w) {
     char* d = static_cast<char*>(dev) + (size_t)r * w;
-    hipError_t x = to_keep ? copy_rows(kp, t * w, d, si * w, t * w, B, kind, s)
-                           : copy_rows(d, si * w, kp, t * w, t * w, B, kind, s);
+    hipError_t x = to_keep ? sppo::launch_copy_rows(kp, t * w, d, si * w, t * w, B, s)
+                           : sppo::launch_copy_rows(d, si * w, kp, t * w, t * w, B, s);
     kp += up(B * t * w);
     return x;
   };
@@ -292,8 +340,8 @@ hipError_t move_keep(sppo_ctx* c, int i, int64_t r, void* q, void* o, float* lse
   if (e == hipSuccess) {  // LSE_i [B, Hq, s_i]: B*Hq spans of t floats
     const size_t BH = B * c->prob.n_q_heads;
     char* d = reinterpret_cast<char*>(lse + r);
-    e = to_keep ? copy_rows(kp, t * 4, d, si * 4, t * 4, BH, kind, s)
-                : copy_rows(d, si * 4, kp, t * 4, t * 4, BH, kind, s);
+    e = to_keep ? sppo::launch_copy_rows(kp, t * 4, d, si * 4, t * 4, BH, s)
+                : sppo::launch_copy_rows(d, si * 4, kp, t * 4, t * 4, BH, s);
     kp += up(BH * t * 4);
   }
   for (size_t k = 0; k < c->extra_rb.size() && e == hipSuccess; ++k) e = plane(extra[k], c->extra_rb[k]);
@@ -347,8 +395,7 @@ void destroy_all(sppo_ctx* c) {
     if (s.base) (void)hipHostFree(s.base);
   }
   if (c->delta) (void)hipFree(c->delta);
-  if (c->d2h) (void)hipStreamDestroy(c->d2h);
-  if (c->h2d) (void)hipStreamDestroy(c->h2d);
+  if (c->d2h) release_copy_streams(c->device);
   delete c;
 }
 
@@ -406,7 +453,9 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
     return fail(nullptr, SPPO_ERR_INVALID_ARG, "n_extra must be 0..16 with extra_row_bytes given");
   }
   for (int k = 0; k < p->n_extra; ++k) {
-    if (p->extra_row_bytes[k] == 0) return fail(nullptr, SPPO_ERR_INVALID_ARG, "extra_row_bytes must be > 0");
+    if (p->extra_row_bytes[k] == 0 || p->extra_row_bytes[k] % 4) {
+      return fail(nullptr, SPPO_ERR_INVALID_ARG, "extra_row_bytes must be positive multiples of 4");
+    }
   }
   if (!(p->softmax_scale >= 0.f) || std::isinf(p->softmax_scale)) {
     return fail(nullptr, SPPO_ERR_INVALID_ARG, "softmax_scale must be finite and >= 0 (0 = 1/sqrt(D))");
@@ -452,9 +501,9 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
     return bail(e == hipErrorOutOfMemory ? SPPO_ERR_OOM : SPPO_ERR_HIP,
                 std::string("hipMalloc(delta): ") + hipGetErrorString(e));
   }
-  if ((e = hipStreamCreateWithFlags(&c->d2h, hipStreamNonBlocking)) != hipSuccess ||
-      (e = hipStreamCreateWithFlags(&c->h2d, hipStreamNonBlocking)) != hipSuccess) {
-    return bail(SPPO_ERR_HIP, std::string("hipStreamCreateWithFlags: ") + hipGetErrorString(e));
+  if ((e = acquire_copy_streams(c->device, &c->d2h, &c->h2d)) != hipSuccess) {
+    c->d2h = c->h2d = nullptr;
+    return bail(SPPO_ERR_HIP, std::string("copy streams: ") + hipGetErrorString(e));
   }
   const int N = p->n_chunks;
   for (auto* v : {&c->ev_fwd, &c->ev_off, &c->ev_call, &c->ev_pf, &c->ev_kv}) {

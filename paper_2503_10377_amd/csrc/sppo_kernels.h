@@ -61,6 +61,12 @@ struct FinalizeArgs {
 };
 hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t stream);
 
+// `height` rows of `width` bytes from src (row pitch spitch) to dst (dpitch),
+// device to device, as a kernel on `stream`.  Widths, pitches and pointers
+// must be multiples of 4 bytes (hipErrorInvalidValue otherwise).
+hipError_t launch_copy_rows(void* dst, size_t dpitch, const void* src, size_t spitch, size_t width, size_t height,
+                            hipStream_t stream);
+
 // Dense bf16 GEMM (fp32 accumulation), C[M, N] (op)= sum_k A(m, k) B(k, n).
 //   tn = 0 (NT): a is [M, K] (row stride lda), b is [N, K] (ldb); K % 64 == 0.
 //   tn = 1 (TN): a is stored [K, M], b is stored [K, N]; M % 256 == 0 and

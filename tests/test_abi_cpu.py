@@ -52,6 +52,7 @@ GOOD = dict(batch=1, seq_len=1024, n_chunks=4, n_q_heads=8, n_kv_heads=2, head_d
     (dict(dtype=7), L.SPPO_ERR_INVALID_ARG),
     (dict(offload=9), L.SPPO_ERR_INVALID_ARG),
     (dict(extra_row_bytes=[16, 0]), L.SPPO_ERR_INVALID_ARG),      # empty extra plane
+    (dict(extra_row_bytes=[16, 6]), L.SPPO_ERR_INVALID_ARG),      # row bytes not a multiple of 4
     (dict(extra_row_bytes=[8] * 17), L.SPPO_ERR_INVALID_ARG),     # too many planes
 ])
 def test_create_rejects_invalid_problems(change, status):

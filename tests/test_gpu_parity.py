@@ -166,3 +166,25 @@ def test_finalize_rounds_each_chunk_after_its_backward(dtype):
         L.sppo_attn_finalize_chunk(ca.ctx, 1, out["dk"], out["dv"], fin["dk"], fin["dk"])
     assert ei.value.status == L.SPPO_ERR_INVALID_ARG
     ca.close()
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_bf16_mqa_ragged_offload(D):
+    """Multi-query attention (8 query heads share one KV head: the dK/dV
+    kernel sums over the whole group), ragged chunks off the tile grid, the
+    full offload set with poisoned dead buffers, and a row-prefix plan with
+    keep buffers on two chunks."""
+    S = 1800
+    offsets = [0, 333, 700, 701, 1500, 1800]
+    lens = [b - a for a, b in zip(offsets, offsets[1:])]
+    rows = [lens[0] // 2, lens[1], 0, lens[3] - 7, 0]
+    gpu, ref, off = run_case(1, S, 8, 1, D, "bf16", offsets=offsets, seed=23, offload="qkvol", poison=True,
+                             rows=rows)
+    check_all(gpu, ref, "bf16", off)
+
+
+def test_bf16_head_dim64_batch3_evict():
+    """head_dim 64, three batch entries, GQA 6/2, the K/V-evicting mode with
+    poisoned cache rows."""
+    gpu, ref, off = run_case(3, 1280, 6, 2, 64, "bf16", N=5, seed=29, offload="qkvol_evict", poison=True)
+    check_all(gpu, ref, "bf16", off)

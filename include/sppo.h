@@ -170,9 +170,10 @@ typedef struct {
  * *out is set only on success.  Errors: INVALID_ARG, UNSUPPORTED, OOM, HIP. */
 sppo_status sppo_create(const sppo_problem* problem, sppo_ctx** out);
 
-/* Synchronise the copy streams and free everything the context owns (the
- * copy streams go when the last context on the device is destroyed).
- * Safe on NULL. */
+/* Synchronise the copy streams (which also waits for copies that other
+ * contexts on the device have enqueued) and free everything the context
+ * owns (the copy streams go when the last context on the device is
+ * destroyed).  Safe on NULL. */
 sppo_status sppo_destroy(sppo_ctx* ctx);
 
 /* Forward of chunk i (Sec. 5.1): for rows r in [c_i, c_{i+1}) and every
@@ -292,9 +293,10 @@ sppo_status sppo_attn_finalize_chunk(sppo_ctx* ctx, int32_t i, const float* dk_a
                                      void* dk_out, void* dv_out, void* stream);
 
 /* Abandon the current forward/backward walk (e.g. after a forward-only run):
- * the next call must be fwd(0).  Blocks until the context's copy streams
- * are idle (copies of the abandoned walk may still read or write its
- * device buffers and host slots), then clears per-chunk offload state. */
+ * the next call must be fwd(0).  Blocks until the device's copy streams are
+ * idle (copies of the abandoned walk may still read or write its device
+ * buffers and host slots; the streams are shared, so this also waits for
+ * copies other contexts have enqueued), then clears per-chunk offload state. */
 sppo_status sppo_reset(sppo_ctx* ctx);
 
 /* Block until the context's copy streams are idle. */

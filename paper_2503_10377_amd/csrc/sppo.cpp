@@ -11,9 +11,10 @@
 // 80 ms per 128K-token step was measured with four contexts alive).  One
 // pair per device keeps the library at two streams whatever the number of
 // contexts (one per layer of a model, say); copies of different contexts
-// then run one after another, as they would on the single host link anyway.  Kernels run on the caller's
-// stream; copies run on the context's streams and are ordered against the
-// caller's stream with events only, so nothing blocks the host.
+// then run one after another, as they would on the single host link anyway.
+// Kernels run on the caller's stream; copies run on the copy streams and are
+// ordered against the caller's stream with events only, so nothing blocks
+// the host.
 //
 // Offload protocol for chunk i (two-level activation management, Sec. 5.1;
 // sequence-aware offloading overlaps chunk i's copy with chunk i+1's

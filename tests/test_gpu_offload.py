@@ -378,3 +378,50 @@ def test_reset_orders_outstanding_copies():
         assert torch.equal(out[name], ref[name]), name
     assert torch.equal(ca.lse_full(out), torch.cat(ref["lse"], dim=2))
     ca.close()
+
+
+def test_contexts_of_a_device_share_the_copy_streams():
+    """Two contexts (two layers of a model, say) whose walks interleave
+    chunk by chunk on one stream: both forward walks, then both backward
+    walks in reverse, every offloaded chunk's Q/O/LSE poisoned once its copy
+    has landed.  The contexts' copies run on the device's one pair of copy
+    streams; each context must still give the bits of its own walk without
+    offload."""
+    S, Hq, Hkv, D, n = SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"], N
+    seeds = (31, 32)
+    refs = [run("none", seed=sd)[0] for sd in seeds]
+    announce("two contexts, interleaved walks on shared copy streams")
+    inps = [make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=sd, device="cuda") for sd in seeds]
+    cas = [ChunkedAttention(1, S, n, Hq, Hkv, D, dtype="bf16", offload="qkvol") for _ in seeds]
+    outs = [ca.alloc_outputs() for ca in cas]
+    qc = [[ca.chunk_view(inp["q"], i) for i in range(n)] for ca, inp in zip(cas, inps)]
+    oc = [[ca.chunk_view(out["o"], i) for i in range(n)] for ca, out in zip(cas, outs)]
+    dc = [[ca.chunk_view(inp["do"], i) for i in range(n)] for ca, inp in zip(cas, inps)]
+    dqc = [[ca.chunk_view(out["dq"], i) for i in range(n)] for ca, out in zip(cas, outs)]
+
+    def bufs(c, i):
+        return L.chunk_bufs(q=qc[c][i], o=oc[c][i], lse=outs[c]["lse"][i], k=inps[c]["k"], v=inps[c]["v"])
+
+    for i in range(n):
+        for c in (0, 1):
+            L.sppo_attn_fwd_chunk(cas[c].ctx, i, qc[c][i], inps[c]["k"], inps[c]["v"], oc[c][i], outs[c]["lse"][i])
+            if i < n - 1:
+                L.sppo_offload_issue(cas[c].ctx, i, bufs(c, i))
+        for c in (0, 1):
+            if i < n - 1:
+                L.sppo_offload_wait(cas[c].ctx, i)
+                qc[c][i].fill_(float("nan"))
+                oc[c][i].fill_(float("nan"))
+                outs[c]["lse"][i].fill_(float("nan"))
+    for i in reversed(range(n)):
+        for c in (1, 0):
+            if 0 <= i - 1 <= n - 2:
+                L.sppo_prefetch(cas[c].ctx, i - 1, bufs(c, i - 1))
+            L.sppo_attn_bwd_chunk(cas[c].ctx, i, qc[c][i], inps[c]["k"], inps[c]["v"], oc[c][i],
+                                  outs[c]["lse"][i], dc[c][i], dqc[c][i], outs[c]["dk"], outs[c]["dv"])
+    torch.cuda.synchronize()
+    for c in (0, 1):
+        got = {"o": outs[c]["o"], "lse": cas[c].lse_full(outs[c]), "dq": outs[c]["dq"],
+               "dk": outs[c]["dk"], "dv": outs[c]["dv"]}
+        assert_bitwise(refs[c], got)
+        cas[c].close()

@@ -25,8 +25,30 @@ BLOCK_ROWS = 4096
 KINDS = ("randn", "sharp_self", "sharp_future", "zero_q")
 
 
+_M32 = 0xFFFFFFFF
+
+
+def _mix32(x: int) -> int:
+    """An invertible mix of 32-bit integers (xor-shifts and odd multipliers,
+    each a bijection), so distinct inputs give distinct outputs."""
+    x ^= x >> 16
+    x = (x * 0x7FEB352D) & _M32
+    x ^= x >> 15
+    x = (x * 0x846CA68B) & _M32
+    return x ^ (x >> 16)
+
+
 def _block_seed(seed: int, tid: int, b: int, blk: int) -> int:
-    return (((seed & 0xFFFF) * 16 + tid) * 65536 + b) * (1 << 20) + blk
+    """64-bit generator seed of one block of one tensor.  (seed, tensor,
+    batch entry, block) are packed into 32 bits and mixed bijectively into
+    both halves: torch's CPU generator keeps only the low 32 bits of a seed
+    (the device generator all 64), so the low half alone must already differ
+    for every block, or on the CPU every tensor would draw the same values."""
+    if not (0 <= seed < 256 and 0 <= tid < 32 and 0 <= b < 8 and 0 <= blk < 65536):
+        raise ValueError(f"seed {seed}, tensor {tid}, batch entry {b} or block {blk} out of the generator's range "
+                         "(seed < 256, batch < 8, sequence < 2^28 rows)")
+    key = (seed << 24) | (tid << 19) | (b << 16) | blk
+    return (_mix32(key ^ 0x5BD1E995) << 32) | _mix32(key)
 
 
 def randn_bshd(shape, seed: int, tid: int, device, dtype) -> torch.Tensor:

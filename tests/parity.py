@@ -50,11 +50,12 @@ def rel_gate_ok(got, ref, dtype):
     return ne <= REL_FRO[dtype] * np.linalg.norm(ref) + REL_FLOOR[dtype] * np.sqrt(got.size)
 
 
-def check(name, got, ref, dtype, offsets=None, axis=1, is_lse=False, scale_abs=False, relative=True):
+def check(name, got, ref, dtype, offsets=None, axis=1, is_lse=False, scale_abs=False, relative=True,
+          max_abs=True):
     """Apply the gates to one tensor; returns the measured figures or raises
     GateError.  ``offsets`` splits ``axis`` into chunks for the per-chunk
     relative gate; ``relative=False`` leaves that gate out (absolute gates
-    only)."""
+    only); ``max_abs=False`` leaves the max-abs gate out (mean-abs only)."""
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     if got.shape != ref.shape:
@@ -71,7 +72,7 @@ def check(name, got, ref, dtype, offsets=None, axis=1, is_lse=False, scale_abs=F
     mx, mean = ABS[dtype]
     if scale_abs and ref.size:
         mx *= max(1.0, float(np.abs(ref).max()))
-    if res["max_abs"] > mx:
+    if max_abs and res["max_abs"] > mx:
         raise GateError(f"{name}: max abs {res['max_abs']:.3e} > {mx}")
     if mean is not None and res["mean_abs"] > mean:
         raise GateError(f"{name}: mean abs {res['mean_abs']:.3e} > {mean}")
@@ -117,7 +118,7 @@ def check_structured(gpu: dict, ref: dict, kind: str, offsets) -> dict:
     sharp_future, zero_q), as tests/test_structured_gates_cpu.py derives
     them from the bf16 recipe emulated on the CPU:
       * the max-abs gate scales with max(1, max|ref|): with sharp_future the
-        recipe's dK reaches 3.4e-2 where max|dK| is 9.5, beyond the
+        recipe's dK reaches 2.3e-2 where max|dK| is 11.7, beyond the
         unscaled 2e-2;
       * with sharp_self, P is nearly one-hot and the exact dQ, dK are tiny
         (max ~1e-2): the recipe's rounding error is of the same size, so

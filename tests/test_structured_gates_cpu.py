@@ -118,3 +118,25 @@ def test_shifted_mask_fails_the_structured_gates(case):
     bad = {n: np.nan_to_num(x, nan=0.0) for n, x in bad.items()}
     with pytest.raises(GateError):
         check_structured(bad, ref, kind, off)
+
+
+def test_sharp_self_over_many_rows_keeps_only_the_mean_gate_on_dq_dk():
+    """The 32K structured test's layout (one query head per KV head) over
+    8192 rows: with Q = 2K a few rows' own keys dominate only weakly (a
+    short key among many), and there dQ and dK are set by the bf16 rounding
+    of the stored O (Delta = dO.O cancels against dP on the diagonal).  The
+    recipe's max error on them passes the 2e-2 gate while the mean stays far
+    under 2e-3, and O, LSE and dV keep the structured gates: what
+    test_seq32k_structured applies to the kind."""
+    S8 = 8192
+    inp = make_inputs(1, S8, 1, 1, D, torch.bfloat16, seed=8, device="cpu", kind="sharp_self")
+    h = {n: t.double().numpy() for n, t in inp.items()}
+    scale = 1 / math.sqrt(D)
+    ref = oracle.attention(h["q"], h["k"], h["v"], h["do"], scale)
+    got = bf16_recipe(h["q"], h["k"], h["v"], h["do"], scale)
+    off = list(oracle.equal_offsets(S8, 2))
+    check_structured({n: got[n] for n in ("o", "dv", "lse")}, ref, "sharp_self", off)
+    for n in ("dq", "dk"):
+        err = np.abs(got[n] - ref[n])
+        assert err.mean() <= 0.25 * 2e-3, (n, err.mean())
+    assert np.abs(got["dk"] - ref["dk"]).max() > 2e-2

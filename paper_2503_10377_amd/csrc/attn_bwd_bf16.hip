@@ -6,12 +6,16 @@
 //   bwd_pre   -Delta_r = -<dO_r, O_r> and LSE2_r = LSE_r * log2(e) into the
 //             context's workspace (HBM-bound); -Delta is the initial value
 //             of the dP accumulators, so the MFMAs produce dP - Delta
-//   bwd_dkdv  one workgroup per 128 keys of one KV head (4 waves x 32 keys,
-//             lane <-> key, K/V fragments in registers); the chunk's query
-//             rows of every head of the GQA group stream through LDS in
+//   bwd_dkdv  one workgroup per 128 keys of one KV head at a time (4 waves x
+//             32 keys, lane <-> key, K/V fragments in registers); the chunk's
+//             query rows of every head of the GQA group stream through LDS in
 //             32-row sub-blocks, and per sub-block
 //               S = Q K^T, dP = dO V^T, P = exp2(S C - LSE2), dS = P (dP - Delta)
 //               dV += P^T dO,  dK += dS^T Q
+//             The kernel is persistent (one workgroup per CU): each XCD
+//             takes key tiles from its own queue, in the XCD-grouped order,
+//             and once it is empty from the other XCDs' queues, so XCDs that
+//             run faster than others do more of the work.
 //   bwd_dq    one workgroup per 128 query rows of one head (lane <-> query);
 //             keys stream through LDS in 32-key sub-blocks, and per sub-block
 //               S^T = K Q^T, dP^T = V dO^T, dS^T as above, dQ^T += K^T dS^T
@@ -56,6 +60,9 @@ __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(ChunkArgs a) {
   const int64_t nrows = a.B * s * a.Hq;
   const int64_t item = ((int64_t)blockIdx.x * 256 + threadIdx.x) / LPI;
   const int sub = threadIdx.x % LPI;
+  // A backward call's queues start from zero (the dK/dV launches leave them
+  // so; cleared here as well, ahead of every call's first dK/dV launch).
+  if (blockIdx.x == 0 && threadIdx.x < 9) atomicExch(a.tiles + threadIdx.x, 0);
   float acc = 0.f;
   if (item < nrows) {
     const u32x4 ov = ld_global16(static_cast<const uint16_t*>(a.o) + item * D + 8 * sub);
@@ -103,7 +110,33 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, g = lane >> 5;
-  const GridPos gp = xcd_grouped();  // the key blocks of a KV head behind one L2
+  // Key tiles in the XCD-grouped order (the tiles of a KV head one after
+  // another): XCD x owns positions [x T / 8, (x+1) T / 8) of the T tiles.
+  // Thread 0 takes the next position from this XCD's queue, or when that
+  // is used up from the next XCD's, and hands it to the workgroup through
+  // LDS; -1 when every queue is used up.
+  const int nx = (int)((a.kv1 - a.kv0 + kKvKeys - 1) / kKvKeys), ny = a.Hkv;
+  const int total = nx * ny * (int)a.B;
+  __shared__ int s_tile;
+  uint32_t xcc;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+  for (;;) {
+  if (tid == 0) {
+    int t = -1;
+    for (int y = 0; y < 8 && t < 0; ++y) {
+      const int x = (int)((xcc + y) & 7);
+      const int lo = (int)((int64_t)x * total / 8), hi = (int)((int64_t)(x + 1) * total / 8);
+      if (lo < hi) {
+        const int n = atomicAdd(a.tiles + x, 1);
+        if (lo + n < hi) t = lo + n;
+      }
+    }
+    s_tile = t;
+  }
+  __syncthreads();
+  const int tile = s_tile;
+  if (tile < 0) break;
+  const GridPos gp{tile % nx, (tile / nx) % ny, tile / (nx * ny)};
   const int hk = gp.y;
   const int64_t b = gp.z;
   const int G = a.Hq / a.Hkv;
@@ -481,6 +514,16 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_kernel(ChunkArgs a) {
       }
     }
   }
+  __syncthreads();  // every wave is past s_tile and the ring before the next tile
+  }
+  // The last workgroup out resets the queues for the next launch (every
+  // other one has taken its last tile before it counts itself out).
+  if (tid == 0) {
+    __threadfence();
+    if (atomicAdd(a.tiles + 8, 1) == (int)gridDim.x - 1) {
+      for (int x = 0; x < 9; ++x) atomicExch(a.tiles + x, 0);
+    }
+  }
 }
 
 // --------------------------------------------------------------------- dQ
@@ -744,6 +787,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_kernel(ChunkArgs a) {
 }  // namespace
 
 hipError_t launch_bwd_pre_bf16(const ChunkArgs& a, hipStream_t stream) {
+  if (!a.tiles) return hipErrorInvalidValue;
   const int64_t s = a.c1 - a.c0;
   const int64_t threads = a.B * s * a.Hq * (a.D / 8);
   dim3 grid((unsigned)((threads + 255) / 256));
@@ -758,8 +802,10 @@ hipError_t launch_bwd_pre_bf16(const ChunkArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_bwd_dkdv_bf16(const ChunkArgs& a, hipStream_t stream) {
-  if (a.kv0 < 0 || a.kv1 > a.c1 || a.kv0 >= a.kv1) return hipErrorInvalidValue;
-  dim3 grid((unsigned)((a.kv1 - a.kv0 + kKvKeys - 1) / kKvKeys), (unsigned)a.Hkv, (unsigned)a.B);
+  if (a.kv0 < 0 || a.kv1 > a.c1 || a.kv0 >= a.kv1 || !a.tiles || a.n_cu < 1) return hipErrorInvalidValue;
+  const int64_t tiles = (a.kv1 - a.kv0 + kKvKeys - 1) / kKvKeys * a.Hkv * a.B;
+  if (tiles > 0x7fffffff) return hipErrorInvalidValue;
+  dim3 grid((unsigned)(tiles < a.n_cu ? tiles : a.n_cu));  // persistent: one workgroup per CU
   if (a.D == 128) {
     hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, grid, dim3(256), 0, stream, a);
   } else if (a.D == 64) {

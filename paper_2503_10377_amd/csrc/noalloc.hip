@@ -11,8 +11,9 @@
 // per device with that device current, and kept.  Every call on one GPU
 // shares that GPU's array: calls that overlap on one GPU (other streams, or
 // other threads) race on it.  Each call's bwd_pre kernel writes every
-// workspace entry its dK/dV and dQ kernels read before they run, so nothing
-// needs clearing between calls.
+// workspace entry its dK/dV and dQ kernels read before they run, and clears
+// the dK/dV kernel's tile queues at the end of the array (which that kernel
+// leaves zero as well), so nothing else needs clearing between calls.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -25,10 +26,13 @@
 namespace {
 
 constexpr size_t kHalf = size_t(1) << 20;  // floats per workspace half: B * Hq * (c1 - c0) <= 2^20
-__device__ __align__(256) float scratch[2 * kHalf];
+// [Delta | LSE2 | dK/dV tile queues]
+__device__ __align__(256) float scratch[2 * kHalf + 64];
+static_assert(sppo::kTileQueueInts * sizeof(int) <= 64 * sizeof(float), "tile queues fit the scratch tail");
 
 constexpr int kMaxDevices = 64;
 float* g_scratch[kMaxDevices] = {};
+int g_n_cu[kMaxDevices] = {};
 std::mutex g_scratch_mu;
 
 sppo_status fail(sppo_status st, const std::string& msg) {
@@ -36,9 +40,10 @@ sppo_status fail(sppo_status st, const std::string& msg) {
   return st;
 }
 
-// Device address of this device's copy of `scratch` (looked up on the
-// first call on each device, with that device current).
-sppo_status scratch_address(float** out) {
+// Device address of this device's copy of `scratch` and the device's
+// compute unit count (looked up on the first call on each device, with that
+// device current).
+sppo_status scratch_address(float** out, int* n_cu) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(SPPO_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
@@ -50,9 +55,16 @@ sppo_status scratch_address(float** out) {
     if (e != hipSuccess || !p) {
       return fail(SPPO_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
     }
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess || cus < 1) {
+      return fail(SPPO_ERR_HIP, std::string("compute unit count: ") + hipGetErrorString(e));
+    }
+    g_n_cu[dev] = cus;
     g_scratch[dev] = static_cast<float*>(p);
   }
   *out = g_scratch[dev];
+  *n_cu = g_n_cu[dev];
   return SPPO_OK;
 }
 
@@ -91,7 +103,8 @@ extern "C" sppo_status sppo_attn_bwd_chunk_noalloc(int64_t batch, int64_t seq_le
                                           " exceeds the static workspace of " + std::to_string(kHalf) + " rows");
   }
   float* ws = nullptr;
-  sppo_status st = scratch_address(&ws);
+  int n_cu = 0;
+  sppo_status st = scratch_address(&ws, &n_cu);
   if (st != SPPO_OK) return st;
 
   sppo::ChunkArgs a{};
@@ -105,6 +118,8 @@ extern "C" sppo_status sppo_attn_bwd_chunk_noalloc(int64_t batch, int64_t seq_le
   a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt((float)head_dim);
   a.delta = ws;
   a.lse2 = ws + kHalf;
+  a.tiles = reinterpret_cast<int*>(ws + 2 * kHalf);
+  a.n_cu = n_cu;
   a.kv0 = 0;
   a.kv1 = c1;
   a.q = q_i;

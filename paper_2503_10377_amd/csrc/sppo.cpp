@@ -71,8 +71,10 @@ struct sppo_ctx {
   size_t elt = 0;
   float scale = 0.f;
   int device = 0;
+  int n_cu = 0;
   hipStream_t d2h = nullptr, h2d = nullptr;
   float* delta = nullptr;
+  int* tiles = nullptr;  // the dK/dV kernel's tile queues, at the end of the delta allocation
   std::vector<HostSlot> slots;
   std::vector<hipEvent_t> ev_fwd, ev_off, ev_call, ev_pf, ev_kv;
   std::vector<EventPair> t_d2h, t_h2d, t_h2d_kv;
@@ -218,6 +220,8 @@ sppo::ChunkArgs make_args(const sppo_ctx* c, int i) {
   a.lse2 = c->delta + (size_t)c->prob.batch * c->prob.n_q_heads * c->s_max;
   a.kv0 = 0;
   a.kv1 = a.c1;
+  a.tiles = c->tiles;
+  a.n_cu = c->n_cu;
   return a;
 }
 
@@ -494,13 +498,23 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
   };
   hipError_t e = hipGetDevice(&c->device);
   if (e != hipSuccess) return bail(SPPO_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
-  // Backward workspace: Delta and LSE * log2(e), [B, Hq, s_max] each.
+  e = hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device);
+  if (e != hipSuccess || c->n_cu < 1) {
+    return bail(SPPO_ERR_HIP, std::string("compute unit count: ") + hipGetErrorString(e));
+  }
+  // Backward workspace: Delta and LSE * log2(e), [B, Hq, s_max] each, then
+  // the dK/dV tile queues (zeroed here; every launch leaves them zero).
   const size_t delta_bytes = (size_t)p->batch * p->n_q_heads * c->s_max * sizeof(float);
-  e = hipMalloc(&c->delta, 2 * delta_bytes);
+  const size_t tiles_off = (2 * delta_bytes + 255) & ~(size_t)255;
+  e = hipMalloc(&c->delta, tiles_off + sppo::kTileQueueInts * sizeof(int));
   if (e != hipSuccess) {
     c->delta = nullptr;
     return bail(e == hipErrorOutOfMemory ? SPPO_ERR_OOM : SPPO_ERR_HIP,
                 std::string("hipMalloc(delta): ") + hipGetErrorString(e));
+  }
+  c->tiles = reinterpret_cast<int*>(reinterpret_cast<char*>(c->delta) + tiles_off);
+  if ((e = hipMemset(c->tiles, 0, sppo::kTileQueueInts * sizeof(int))) != hipSuccess) {
+    return bail(SPPO_ERR_HIP, std::string("hipMemset(tile queues): ") + hipGetErrorString(e));
   }
   if ((e = acquire_copy_streams(c->device, &c->d2h, &c->h2d)) != hipSuccess) {
     c->d2h = c->h2d = nullptr;

@@ -32,7 +32,14 @@ struct ChunkArgs {
   float scale;
   int accumulate;      // dk/dv: 0 = overwrite rows [kv0, kv1), 1 = add
   int64_t kv0, kv1;    // dkdv: key rows computed, a sub-range of [0, c1)
+  int* tiles;          // bf16 dkdv: tile queues, kTileQueueInts ints, zero between launches
+  int n_cu;            // compute units of the device (bf16 dkdv: one workgroup each)
 };
+
+// The bf16 dK/dV kernel takes its key tiles from one queue per XCD (a
+// counter each, [0, 8)) and counts its finished workgroups ([8]); the last
+// one resets all nine, so every launch on a stream starts from zero.
+constexpr int kTileQueueInts = 16;
 
 // Each launcher enqueues one kernel on `stream` and returns the launch
 // status.  The backward of a chunk is pre (Delta), then dkdv (one launch for

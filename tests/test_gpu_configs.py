@@ -90,7 +90,19 @@ def run_full(S, N, Hq, Hkv, D, offload, seed=0, poison=False, kind="randn"):
     return inp, res, offsets
 
 
-def check_sampled_rows(inp, res, offsets, groups, rows, Hq, Hkv, D):
+def gate_kw(kind, name):
+    """Gate options for a tensor: the bf16 gates for N(0,1) inputs; for the
+    structured kinds check_structured's (max-abs scaled by max(1, max|ref|)),
+    with sharp_self's dQ and dK over long sequences on the mean-abs gate
+    only (see check_full_heads)."""
+    if kind is None:
+        return {}
+    if kind == "sharp_self" and name in ("dq", "dk"):
+        return {"scale_abs": True, "relative": False, "max_abs": False}
+    return {"scale_abs": True}
+
+
+def check_sampled_rows(inp, res, offsets, groups, rows, Hq, Hkv, D, kind=None):
     G = Hq // Hkv
     scale = 1 / math.sqrt(D)
 
@@ -108,14 +120,14 @@ def check_sampled_rows(inp, res, offsets, groups, rows, Hq, Hkv, D):
     with cf.ThreadPoolExecutor(THREADS) as ex:
         for g, ref, got in ex.map(one, groups):
             for n in ("o", "dq"):
-                r = check(f"{n}[g{g}]", got[n], ref[n], "bf16")
+                r = check(f"{n}[g{g}]", got[n], ref[n], "bf16", **gate_kw(kind, n))
                 worst[n] = max(worst.get(n, 0), r["max_abs"])
             r = check(f"lse[g{g}]", got["lse"], ref["lse"], "bf16", is_lse=True)
             worst["lse"] = max(worst.get("lse", 0), r["max_abs"])
     return worst
 
 
-def check_tail_keys(inp, res, groups, T, S, Hq, Hkv, D):
+def check_tail_keys(inp, res, groups, T, S, Hq, Hkv, D, kind=None):
     G = Hq // Hkv
     scale = 1 / math.sqrt(D)
     t0 = S - T
@@ -130,8 +142,10 @@ def check_tail_keys(inp, res, groups, T, S, Hq, Hkv, D):
     announce(f"oracle: last {T} keys x groups {list(groups)}")
     with cf.ThreadPoolExecutor(THREADS) as ex:
         for g, dk, dv in ex.map(one, groups):
-            check(f"dk_tail[g{g}]", res["dk"][:, t0:, g:g + 1].double().cpu().numpy(), dk, "bf16")
-            check(f"dv_tail[g{g}]", res["dv"][:, t0:, g:g + 1].double().cpu().numpy(), dv, "bf16")
+            check(f"dk_tail[g{g}]", res["dk"][:, t0:, g:g + 1].double().cpu().numpy(), dk, "bf16",
+                  **gate_kw(kind, "dk"))
+            check(f"dv_tail[g{g}]", res["dv"][:, t0:, g:g + 1].double().cpu().numpy(), dv, "bf16",
+                  **gate_kw(kind, "dv"))
 
 
 def check_keys(inp, res, groups, keys, S, Hq, Hkv, D, rows_per_task=1024, row_block=128):
@@ -277,6 +291,21 @@ def test_seq128k_16chunks_offload():
     early += rng.integers(0, off[N - 1], 56).tolist()
     check_keys(inp, res, (0, Hkv - 1), early, S, Hq, Hkv, D)
     check_invariants(inp, res, Hq, Hkv)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("kind", ["sharp_self", "sharp_future"])
+def test_seq128k_structured_offload(kind):
+    """Structured inputs at 128K in the benchmark's walk (offload, poisoned
+    dead buffers): sharp_self would expose a mask that hides a row's own
+    key, sharp_future one that admits the next key, at every chunk boundary
+    and tile edge of the sampled rows, for positions up to 128K; and the
+    last keys' dK/dV."""
+    S, N, Hq, Hkv, D = 131072, 16, 32, 32, 128
+    inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=9, poison=True, kind=kind)
+    rng = np.random.default_rng(5)
+    check_sampled_rows(inp, res, off, (0, Hkv - 1), sample_rows(off, S, 16, rng), Hq, Hkv, D, kind=kind)
+    check_tail_keys(inp, res, (0, Hkv - 1), 256, S, Hq, Hkv, D, kind=kind)
 
 
 @pytest.mark.timeout(1200)

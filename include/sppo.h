@@ -339,9 +339,10 @@ sppo_status sppo_prefetch_wait(sppo_ctx* ctx, int32_t i, void* stream);
  * capture, tight serving loops, harnesses that forbid hipMalloc): the
  * backward of one chunk [c0, c1) as sppo_attn_bwd_chunk enqueues it (same
  * kernels, same results bit for bit), without a context and without any
- * allocation.  Its Delta / LSE workspace is a static device array of the
- * library (8 MiB on every GPU the library runs on, held until the process
- * ends), so batch * n_q_heads * (c1 - c0) must not exceed 2^20
+ * allocation.  Its Delta / LSE workspace and the dK/dV kernel's tile
+ * queues are a static device array of the library (8 MiB on every GPU the
+ * library runs on, held until the process ends; the queues are cleared by
+ * each call and left zero), so batch * n_q_heads * (c1 - c0) must not exceed 2^20
  * (UNSUPPORTED otherwise).  Every call on one GPU shares that GPU's array:
  * calls that overlap on one GPU (several streams or threads) race, so the
  * caller orders them (e.g. one stream).  Arguments as in sppo_create and

@@ -425,3 +425,60 @@ def test_contexts_of_a_device_share_the_copy_streams():
                "dk": outs[c]["dk"], "dv": outs[c]["dv"]}
         assert_bitwise(refs[c], got)
         cas[c].close()
+
+
+class _Serializer:
+    """Stands in for the walk's host pacer: at every chunk boundary the host
+    waits until the device, the copy streams included, is idle."""
+
+    def __init__(self, ctx):
+        self.ctx = ctx
+
+    def boundary(self, stream):
+        torch.cuda.synchronize()
+        L.sppo_sync(self.ctx)
+
+
+@pytest.mark.parametrize("mode", ["qkvol", "qkvol_evict"])
+def test_serialized_walk_matches_the_overlapped_one(mode):
+    """The same offloading walk with every chunk's work finished (kernels and
+    copies) before the next chunk's calls are made, against the walk where
+    copies overlap compute: bitwise equal, so no result depends on how the
+    copies interleave with the kernels."""
+    announce(f"serialized vs overlapped walk, {mode}")
+    res = {}
+    for name in ("overlapped", "serialized"):
+        inp = make_inputs(1, SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"], torch.bfloat16, seed=23,
+                          device="cuda")
+        ca = ChunkedAttention(1, SHAPE["S"], N, SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"], dtype="bf16", offload=mode)
+        if name == "serialized":
+            ca.pacer = _Serializer(ca.ctx)
+        out = ca.alloc_outputs()
+        ca.step(inp, out, poison=True)
+        torch.cuda.synchronize()
+        res[name] = {"o": out["o"].clone(), "lse": ca.lse_full(out).clone(), "dq": out["dq"].clone(),
+                     "dk": out["dk"].clone(), "dv": out["dv"].clone()}
+        ca.close()
+    assert_bitwise(res["overlapped"], res["serialized"])
+
+
+def test_competing_link_traffic_leaves_results_unchanged():
+    """The walk's copies share the host link with large copies of another
+    stream, so they land later than they would alone: the backward still
+    waits for each prefetch (poisoned dead buffers) and every result stays
+    bitwise equal to the walk without offload."""
+    announce("walk beside 1 GiB copies on another stream")
+    ref, _ = run("none", seed=29)
+    nbytes = 1 << 30
+    dev = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    host = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    bg = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(bg):
+        for _ in range(3):
+            host.copy_(dev, non_blocking=True)
+            dev.copy_(host, non_blocking=True)
+    res, _ = run("qkvol", seed=29, poison=True, lookahead=1)
+    torch.cuda.synchronize()
+    assert_bitwise(ref, res)
+    del dev, host

@@ -482,3 +482,29 @@ def test_competing_link_traffic_leaves_results_unchanged():
     torch.cuda.synchronize()
     assert_bitwise(ref, res)
     del dev, host
+
+
+def test_contexts_on_two_streams_run_concurrently():
+    """Two contexts' offloading walks, each on its own stream and enqueued
+    back to back with the host unpaced, so their kernels and copies run on
+    the device at the same time (each dK/dV launch with its own context's
+    tile queues): each gives the bits of its walk run alone."""
+    seeds = (41, 42)
+    shape = (32768, 8, 2, 128)  # a few ms of device time per walk, so the walks overlap
+    refs = [run("qkvol", seed=sd, shape=shape)[0] for sd in seeds]
+    announce("two contexts on two streams at once")
+    S, Hq, Hkv, D = shape
+    inps = [make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=sd, device="cuda") for sd in seeds]
+    cas = [ChunkedAttention(1, S, N, Hq, Hkv, D, dtype="bf16", offload="qkvol", host_ahead=0) for _ in seeds]
+    outs = [ca.alloc_outputs() for ca in cas]
+    for ca in cas:
+        ca.prepare()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for ca, inp, out, st in zip(cas, inps, outs, streams):
+        ca.step(inp, out, poison=True, stream=st)
+    torch.cuda.synchronize()
+    for ref, ca, out in zip(refs, cas, outs):
+        got = {"o": out["o"], "lse": ca.lse_full(out), "dq": out["dq"], "dk": out["dk"], "dv": out["dv"]}
+        assert_bitwise(ref, got)
+        ca.close()

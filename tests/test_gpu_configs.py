@@ -311,9 +311,15 @@ def test_seq128k_structured_offload(kind):
 @pytest.mark.timeout(1200)
 def test_seq512k_32chunks_gqa_offload():
     """bf16 GQA, 32 query / 8 KV heads x 128, seq 524288 in 32 chunks of
-    16384, per-chunk offload/prefetch."""
+    16384, per-chunk offload/prefetch.  The same walk with the K/V cache
+    evicted after the forward walk (and poisoned) must give the same bits."""
     S, N, Hq, Hkv, D = 524288, 32, 32, 8, 128
+    _, ev, _ = run_full(S, N, Hq, Hkv, D, "qkvol_evict", seed=0, poison=True)
     inp, res, off = run_full(S, N, Hq, Hkv, D, "qkvol", seed=0, poison=True)
+    announce("evicting walk == resident walk, bitwise")
+    for n in res:
+        assert torch.equal(res[n], ev[n]), n
+    del ev
     rng = np.random.default_rng(3)
     check_sampled_rows(inp, res, off, (0, Hkv - 1), sample_rows(off, S, 16, rng, every=4), Hq, Hkv, D)
     check_sampled_rows(inp, res, off, range(Hkv), np.array(sorted(rng.integers(0, S, 4))), Hq, Hkv, D)

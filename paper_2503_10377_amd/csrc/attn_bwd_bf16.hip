@@ -12,7 +12,8 @@
 //             32-row sub-blocks, and per sub-block
 //               S = Q K^T, dP = dO V^T, P = exp2(S C - LSE2), dS = P (dP - Delta)
 //               dV += P^T dO,  dK += dS^T Q
-//             The kernel is persistent (one workgroup per CU): each XCD
+//             The kernel is persistent (as many workgroups as the CUs
+//             hold at once, one per CU at its register use): each XCD
 //             takes key tiles from its own queue, in the XCD-grouped order,
 //             and once it is empty from the other XCDs' queues, so XCDs that
 //             run faster than others do more of the work.
@@ -801,17 +802,33 @@ hipError_t launch_bwd_pre_bf16(const ChunkArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// Workgroups of the persistent dK/dV kernel that one CU holds at once (its
+// registers allow one; asked of the runtime once per head size).
+template <int D>
+int dkdv_groups_per_cu() {
+  static const int n = [] {
+    int b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, reinterpret_cast<const void*>(&bwd_dkdv_bf16_kernel<D>),
+                                                     256, 0) != hipSuccess || b < 1) {
+      b = 1;
+    }
+    return b;
+  }();
+  return n;
+}
+
 hipError_t launch_bwd_dkdv_bf16(const ChunkArgs& a, hipStream_t stream) {
   if (a.kv0 < 0 || a.kv1 > a.c1 || a.kv0 >= a.kv1 || !a.tiles || a.n_cu < 1) return hipErrorInvalidValue;
+  if (a.D != 128 && a.D != 64) return hipErrorInvalidValue;
   const int64_t tiles = (a.kv1 - a.kv0 + kKvKeys - 1) / kKvKeys * a.Hkv * a.B;
   if (tiles > 0x7fffffff) return hipErrorInvalidValue;
-  dim3 grid((unsigned)(tiles < a.n_cu ? tiles : a.n_cu));  // persistent: one workgroup per CU
+  // persistent: as many workgroups as the CUs hold at once
+  const int64_t slots = (int64_t)a.n_cu * (a.D == 128 ? dkdv_groups_per_cu<128>() : dkdv_groups_per_cu<64>());
+  dim3 grid((unsigned)(tiles < slots ? tiles : slots));
   if (a.D == 128) {
     hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, grid, dim3(256), 0, stream, a);
-  } else if (a.D == 64) {
-    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<64>, grid, dim3(256), 0, stream, a);
   } else {
-    return hipErrorInvalidValue;
+    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<64>, grid, dim3(256), 0, stream, a);
   }
   return hipGetLastError();
 }

@@ -85,7 +85,9 @@ typedef enum {
 } sppo_offload;
 
 /* The problem, in the paper's notation (B, S, N, s_i) plus the attention
- * shape (query heads, KV heads, head dim).  Copied by sppo_create. */
+ * shape (query heads, KV heads, head dim).  Copied by sppo_create, which
+ * returns UNSUPPORTED when B or a head count exceeds 65535 or a
+ * [B, S, max(Hq, Hkv), D] tensor would exceed 2^62 bytes. */
 typedef struct {
   int64_t batch;                 /* B >= 1                                  */
   int64_t seq_len;               /* 1 <= S < 2^31 (kernels index keys in int) */
@@ -343,7 +345,7 @@ sppo_status sppo_prefetch_wait(sppo_ctx* ctx, int32_t i, void* stream);
  * queues are a static device array of the library (8 MiB on every GPU the
  * library runs on, held until the process ends; the queues are cleared by
  * each call and left zero), so batch * n_q_heads * (c1 - c0) must not exceed 2^20
- * (UNSUPPORTED otherwise).  Every call on one GPU shares that GPU's array:
+ * (UNSUPPORTED otherwise, as for the size limits of sppo_create).  Every call on one GPU shares that GPU's array:
  * calls that overlap on one GPU (several streams or threads) race, so the
  * caller orders them (e.g. one stream).  Arguments as in sppo_create and
  * sppo_attn_bwd_chunk: q_i, o_i, do_i, dq_i [B, c1 - c0, Hq, D] and lse_i

@@ -16,6 +16,7 @@
 // leaves zero as well), so nothing else needs clearing between calls.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <mutex>
 #include <string>
@@ -87,6 +88,9 @@ extern "C" sppo_status sppo_attn_bwd_chunk_noalloc(int64_t batch, int64_t seq_le
     return fail(SPPO_ERR_INVALID_ARG, "need 0 <= c0 < c1 <= seq_len < 2^31");
   }
   if (head_dim != 64 && head_dim != 128) return fail(SPPO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if ((double)batch * (double)seq_len * (double)std::max(n_q_heads, n_kv_heads) * (double)head_dim * 4.0 > 0x1p62) {
+    return fail(SPPO_ERR_UNSUPPORTED, "a [B, S, H, D] tensor of this problem would exceed 2^62 bytes");
+  }
   if (dtype != SPPO_F32 && dtype != SPPO_BF16) return fail(SPPO_ERR_INVALID_ARG, "unknown dtype");
   if (!(softmax_scale >= 0.f) || std::isinf(softmax_scale)) {
     return fail(SPPO_ERR_INVALID_ARG, "softmax_scale must be finite and >= 0 (0 = 1/sqrt(D))");

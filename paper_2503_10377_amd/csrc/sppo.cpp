@@ -450,6 +450,12 @@ sppo_status sppo_create(const sppo_problem* p, sppo_ctx** out) {
   if (p->head_dim != 64 && p->head_dim != 128) {
     return fail(nullptr, SPPO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
   }
+  // Sizes and offsets are 64-bit products of these counts: keep every
+  // [B, S, H, D] tensor (and so the workspace and host slots) below 2^62 bytes.
+  if ((double)p->batch * (double)p->seq_len * (double)std::max(p->n_q_heads, p->n_kv_heads) *
+          (double)p->head_dim * 4.0 > 0x1p62) {
+    return fail(nullptr, SPPO_ERR_UNSUPPORTED, "a [B, S, H, D] tensor of this problem would exceed 2^62 bytes");
+  }
   if (p->offload != SPPO_OFFLOAD_NONE && p->offload != SPPO_OFFLOAD_QOL && p->offload != SPPO_OFFLOAD_QKVOL &&
       p->offload != SPPO_OFFLOAD_QKVOL_EVICT) {
     return fail(nullptr, SPPO_ERR_INVALID_ARG, "unknown offload mode");

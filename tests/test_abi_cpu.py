@@ -39,6 +39,10 @@ GOOD = dict(batch=1, seq_len=1024, n_chunks=4, n_q_heads=8, n_kv_heads=2, head_d
     (dict(head_dim=96), L.SPPO_ERR_UNSUPPORTED),
     (dict(head_dim=0), L.SPPO_ERR_UNSUPPORTED),
     (dict(seq_len=2**31, n_chunks=1), L.SPPO_ERR_UNSUPPORTED),   # key indices are int32
+    (dict(batch=65535, seq_len=2**31 - 1, n_chunks=1, n_q_heads=65535, n_kv_heads=65535),
+     L.SPPO_ERR_UNSUPPORTED),                                     # tensor bytes beyond 2^62
+    (dict(batch=4096, seq_len=2**30, n_chunks=1, n_q_heads=4096, n_kv_heads=4096),
+     L.SPPO_ERR_UNSUPPORTED),
     (dict(n_kv_heads=3), L.SPPO_ERR_INVALID_ARG),
     (dict(n_kv_heads=0), L.SPPO_ERR_INVALID_ARG),
     (dict(batch=0), L.SPPO_ERR_INVALID_ARG),
@@ -114,6 +118,7 @@ def test_layer_ops_reject_invalid_arguments_before_launch():
 
 @pytest.mark.parametrize("change,status", [
     (dict(S=65536, c1=65536, Hq=32), L.SPPO_ERR_UNSUPPORTED),  # B * Hq * (c1 - c0) > 2^20 workspace rows
+    (dict(B=65535, S=2**31 - 1, c1=1, Hq=65535, Hkv=65535), L.SPPO_ERR_UNSUPPORTED),  # tensor bytes beyond 2^62
     (dict(D=96), L.SPPO_ERR_UNSUPPORTED),
     (dict(c0=10, c1=10), L.SPPO_ERR_INVALID_ARG),
     (dict(c1=5000), L.SPPO_ERR_INVALID_ARG),             # past seq_len

@@ -188,3 +188,12 @@ def test_bf16_head_dim64_batch3_evict():
     poisoned cache rows."""
     gpu, ref, off = run_case(3, 1280, 6, 2, 64, "bf16", N=5, seed=29, offload="qkvol_evict", poison=True)
     check_all(gpu, ref, "bf16", off)
+
+
+@pytest.mark.parametrize("offload", ["qkvol", "qkvol_evict"])
+def test_bf16_every_chunk_one_row(offload):
+    """N = S: every chunk is one query row (a 31-row padded sub-block in
+    every kernel, one-row copies of each tensor), offloaded and poisoned,
+    over a walk of 48 chunks."""
+    gpu, ref, off = run_case(1, 48, 4, 2, 128, "bf16", N=48, seed=31, offload=offload, poison=True)
+    check_all(gpu, ref, "bf16", off)

@@ -46,7 +46,7 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& x) { return __builtin_b
 
 __device__ __forceinline__ u32x4 ld_global16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 
-// Round 8 floats to bf16 (round-to-nearest-even, v_cvt_pk_bf16_f32).
+// Eight floats to bf16, rounded to nearest even (v_cvt_pk_bf16_f32).
 __device__ __forceinline__ bf16x8 pack_bf16x8(float x0, float x1, float x2, float x3, float x4,
                                               float x5, float x6, float x7) {
   bf16x8 r;

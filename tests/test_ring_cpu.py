@@ -75,3 +75,53 @@ def test_every_schedule_replays_at_its_capacity(N, lookahead, which, sizes):
     total = sum(R._up(s) for s in sz)
     # circular first fit can fragment around chunks that stay resident
     assert cap <= (total if which != "some" else total + max(R._up(s) for s in sz))
+
+
+# ---- property test: the circular allocator against an independent model ----
+from hypothesis import given, settings, strategies as st
+
+
+@settings(max_examples=300, deadline=None)
+@given(cap_blocks=st.integers(1, 24), q=st.integers(0, 3),
+       ops=st.lists(st.tuples(st.sampled_from(["alloc", "release"]), st.integers(1, 8 * R.ALIGN),
+                              st.integers(0, 10 ** 6), st.booleans()), max_size=60))
+def test_allocator_against_a_model(cap_blocks, q, ops):
+    """Random allocations and releases.  A model of the byte ranges (live,
+    released by an offload at allocation count t, or free) checks every
+    answer: placements in bounds and aligned, never over a live range or an
+    offloaded one inside its quarantine; every offloaded range a placement
+    reuses is reported through ``take`` (the caller waits for its copy);
+    a failed allocation means no aligned placement was possible; the bytes
+    in use match the live ranges."""
+    cap = cap_blocks * R.ALIGN
+    a = R.CircularAllocator(cap)
+    model = []  # [start, end, state, released_at]
+
+    def usable(r, count):  # count: the allocations made before the one asking
+        return r[2] == "free" or (r[2] == "offload" and count - r[3] >= q)
+
+    for kind, nbytes, pick, offl in ops:
+        if kind == "alloc":
+            n = R._up(nbytes)
+            before = a.count
+            taken = []
+            off = a.alloc(nbytes, 0, lambda reg: a.count - reg.released_at >= q, lambda reg: taken.append(reg.start))
+            if off is None:
+                for s in range(0, cap - n + 1, R.ALIGN):
+                    assert any(m[0] < s + n and m[1] > s and not usable(m, before) for m in model), (s, n, model)
+                assert a.count == before
+                continue
+            assert off % R.ALIGN == 0 and 0 <= off and off + n <= cap
+            over = [m for m in model if m[0] < off + n and m[1] > off]
+            assert all(usable(m, before) for m in over), (off, n, over)
+            assert sorted(taken) == sorted(m[0] for m in over if m[2] == "offload")
+            model = [m for m in model if m not in over] + [[off, off + n, "live", 0]]
+        else:
+            live = [m for m in model if m[2] == "live"]
+            if not live:
+                continue
+            m = live[pick % len(live)]
+            a.release(m[0], after_offload=offl)
+            m[2], m[3] = ("offload" if offl else "free"), a.count
+        assert a.in_use == sum(m[1] - m[0] for m in model if m[2] == "live")
+        assert a.high_water >= a.in_use

@@ -38,30 +38,40 @@ def bf16(x):
     return torch.from_numpy(np.ascontiguousarray(x)).float().to(torch.bfloat16).double().numpy()
 
 
-def bf16_recipe(q, k, v, do, scale):
+def _exp(x):
+    """fp64 exp on all host threads (numpy's runs on one)."""
+    return torch.from_numpy(x).exp().numpy()
+
+
+def bf16_recipe(q, k, v, do, scale, row_block=1024):
+    """The kernels' bf16 rounding points on fp64 arithmetic, a block of query
+    rows at a time (each block against the keys it can see; hidden pairs add
+    exact zeros, so the blocking changes only the fp64 summation order)."""
     B, S_, H, _ = q.shape
     G = H // k.shape[2]
     out = {"o": np.zeros_like(q), "lse": np.zeros((B, H, S_)), "dq": np.zeros_like(q),
            "dk": np.zeros_like(k), "dv": np.zeros_like(v)}
-    hidden = np.arange(S_)[None, :] > np.arange(S_)[:, None]
     for b in range(B):
         for h in range(H):
             g = h // G
             qh, kh, vh, doh = q[b, :, h], k[b, :, g], v[b, :, g], do[b, :, h]
-            s = scale * (qh @ kh.T)
-            s[hidden] = -np.inf
-            m = s.max(axis=1, keepdims=True)
-            p = np.exp(s - m)
-            l_ = p.sum(axis=1, keepdims=True)
-            o = bf16((bf16(p) @ vh) / l_)
-            lse = (m + np.log(l_))[:, 0]
-            delta = (doh * o).sum(axis=1)
-            P = np.exp(s - lse[:, None])
-            dS = P * (doh @ vh.T - delta[:, None])
-            out["o"][b, :, h], out["lse"][b, h] = o, lse
-            out["dv"][b, :, g] += bf16(P).T @ doh
-            out["dq"][b, :, h] = bf16(scale * (bf16(dS) @ kh))
-            out["dk"][b, :, g] += scale * (bf16(dS).T @ qh)
+            for r0 in range(0, S_, row_block):
+                r1 = min(S_, r0 + row_block)
+                kb, vb, qb, dob = kh[:r1], vh[:r1], qh[r0:r1], doh[r0:r1]
+                s = scale * (qb @ kb.T)
+                s[np.arange(r1)[None, :] > np.arange(r0, r1)[:, None]] = -np.inf
+                m = s.max(axis=1, keepdims=True)
+                p = _exp(s - m)
+                l_ = p.sum(axis=1, keepdims=True)
+                o = bf16((bf16(p) @ vb) / l_)
+                lse = (m + np.log(l_))[:, 0]
+                delta = (dob * o).sum(axis=1)
+                P = _exp(s - lse[:, None])
+                dS = bf16(P * (dob @ vb.T - delta[:, None]))
+                out["o"][b, r0:r1, h], out["lse"][b, h, r0:r1] = o, lse
+                out["dv"][b, :r1, g] += bf16(P).T @ dob
+                out["dq"][b, r0:r1, h] = bf16(scale * (dS @ kb))
+                out["dk"][b, :r1, g] += scale * (dS.T @ qb)
     return out
 
 

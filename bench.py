@@ -404,7 +404,7 @@ def main():
     ap.add_argument("--layer", action="store_true",
                     help="instead of the headline line: the full-layer chunk walk (projections, attention, MLP) "
                          "at seq 131072 in 16 chunks, width 4096")
-    ap.add_argument("--layer-offload", default="qol", choices=("none", "qol", "qkvol"))
+    ap.add_argument("--layer-offload", default="qol", choices=("none", "qol", "qkvol", "qkvol_evict"))
     ap.add_argument("--layer-cpu-tokens", type=int, default=4096)
     args = ap.parse_args()
     if args.copy_calibration:

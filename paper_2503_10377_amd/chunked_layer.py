@@ -15,7 +15,9 @@ sequence stays on the device; every other tensor a chunk's backward needs --
 Q_i, O_i, LSE_i and the "extra planes" x_i, h_i, a_i and the two
 LayerNorms' statistics -- is offloaded after the chunk's forward (all chunks
 but the last by default) and prefetched before its backward.  u, z and
-gelu(a) are recomputed in the backward from x, h and a.
+gelu(a) are recomputed in the backward from x, h and a.  With
+``qkvol_evict`` the offloaded chunks' K/V cache rows are given up after the
+forward walk as well and stream back under the last chunk's backward.
 
 The saved tensors a chunk produces live in a region of a preallocated
 device arena (ring.DeviceArena): an offloaded chunk's region is reused once
@@ -243,6 +245,23 @@ class ChunkedLayer:
             else:
                 held[i] = (slot, v)
         fwd_phase[0] = False
+        if self.offload == L.SPPO_OFFLOAD_QKVOL_EVICT:
+            # The K/V cache rows of the offloaded chunks are given up here;
+            # their copies come back on the host-to-device stream in the order
+            # the last chunk's backward consumes them (chunk by chunk).
+            rows = L.sppo_get_offload_rows(self.ctx)
+            kv_chunks = sorted(offl, reverse=True)
+            if poison:
+                # Test hook: the evicted rows are dead once their copies have landed.
+                for j in kv_chunks:
+                    L.sppo_offload_wait(self.ctx, j, s)
+                with torch.cuda.stream(s):
+                    for j in kv_chunks:
+                        c0 = self.offsets[j]
+                        self.k[c0:c0 + rows[j]].fill_(float("nan"))
+                        self.v[c0:c0 + rows[j]].fill_(float("nan"))
+            for j in kv_chunks:
+                L.sppo_prefetch_kv(self.ctx, j, self.k, self.v, s)
         pending = sorted(offl, reverse=True)
         nxt = 0
         for i in reversed(range(self.N)):

@@ -78,10 +78,12 @@ def test_layer_matches_oracle(Hq, Hkv, D, offsets):
     check(got, oracle_layer(host, Hq, Hkv, D))
 
 
-@pytest.mark.parametrize("offload,rows", [("qol", None), ("qkvol", [200, 0, 1, 512])])
+@pytest.mark.parametrize("offload,rows", [("qol", None), ("qkvol", [200, 0, 1, 512]), ("qkvol_evict", None),
+                                          ("qkvol_evict", [200, 0, 1, 512])])
 def test_layer_offload_is_bitwise_invisible(offload, rows):
     # Q/O/LSE and the extra planes (x, h, a, LayerNorm statistics) of the
-    # offloaded chunks are poisoned on the device once copied out.
+    # offloaded chunks are poisoned on the device once copied out; with
+    # qkvol_evict so are their K/V cache rows after the forward walk.
     offsets = [0, 256, 512, 768, 1024]
     if rows is not None:
         rows = [min(r, offsets[i + 1] - offsets[i]) for i, r in enumerate(rows)]

@@ -197,3 +197,16 @@ def test_bf16_every_chunk_one_row(offload):
     over a walk of 48 chunks."""
     gpu, ref, off = run_case(1, 48, 4, 2, 128, "bf16", N=48, seed=31, offload=offload, poison=True)
     check_all(gpu, ref, "bf16", off)
+
+
+@pytest.mark.parametrize("offload", ["qkvol", "qkvol_evict"])
+def test_fp32_offload_row_prefix_batch2(offload):
+    """The fp32 path through the offload engine (4-byte elements in every
+    copy, keep buffer and arena region): batch 2, GQA, ragged chunks, a
+    row-prefix plan with keep buffers, poisoned dead buffers."""
+    offsets = [0, 97, 300, 301, 640]
+    lens = [b - a for a, b in zip(offsets, offsets[1:])]
+    rows = [lens[0] - 10, 0, 1, lens[3]]
+    gpu, ref, off = run_case(2, 640, 4, 2, 64, "f32", offsets=offsets, seed=37, offload=offload, poison=True,
+                             rows=rows)
+    check_all(gpu, ref, "f32", off)

@@ -24,7 +24,7 @@ def announce(msg):
 
 
 def run_case(B, S, Hq, Hkv, D, dtype, N=None, offsets=None, seed=0, kind="randn",
-             offload="none", lookahead=2, poison=False, rows=None):
+             offload="none", lookahead=2, poison=False, rows=None, softmax_scale=None):
     if offsets is None:
         offsets = list(oracle.equal_offsets(S, N))
     N = len(offsets) - 1
@@ -32,7 +32,8 @@ def run_case(B, S, Hq, Hkv, D, dtype, N=None, offsets=None, seed=0, kind="randn"
              f"seed={seed} kind={kind} offload={offload} poison={poison}")
     inp = make_inputs(B, S, Hq, Hkv, D, TORCH_DT[dtype], seed=seed, device="cuda", kind=kind)
     host = {n: to_np(t) for n, t in inp.items()}  # taken before the HIP path runs
-    ca = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype=dtype, offsets=offsets, offload=offload)
+    ca = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype=dtype, offsets=offsets, offload=offload,
+                          scale=softmax_scale or 0.0)
     if rows is not None:
         ca.set_offload_rows(rows)
     out = ca.alloc_outputs()
@@ -41,7 +42,7 @@ def run_case(B, S, Hq, Hkv, D, dtype, N=None, offsets=None, seed=0, kind="randn"
     gpu = {"o": to_np(out["o"]), "lse": to_np(ca.lse_full(out)), "dq": to_np(out["dq"]),
            "dk": to_np(out["dk"]), "dv": to_np(out["dv"])}
     ca.close()
-    scale = 1.0 / math.sqrt(D)
+    scale = softmax_scale or 1.0 / math.sqrt(D)
     ref = oracle.attention(host["q"], host["k"], host["v"], host["do"], scale)
     return gpu, ref, offsets
 
@@ -210,3 +211,16 @@ def test_fp32_offload_row_prefix_batch2(offload):
     gpu, ref, off = run_case(2, 640, 4, 2, 64, "f32", offsets=offsets, seed=37, offload=offload, poison=True,
                              rows=rows)
     check_all(gpu, ref, "f32", off)
+
+
+@pytest.mark.parametrize("dtype,scale", [("bf16", 0.15), ("f32", 0.2)])
+def test_explicit_softmax_scale(dtype, scale):
+    """A softmax scale other than 1/sqrt(D) (0.088 at D = 128) reaches every
+    kernel: the forward's exponent, the backward's recomputed P, and the
+    scale on dQ and dK.  Ragged GQA chunks, offloaded and poisoned.  (The
+    fp32 LSE gate, 1e-5 absolute, is sized for logits of the default scale:
+    the fp32 rounding of a 128-term dot product grows with the scale, and at
+    0.5, logits around 20, it reaches 1.3e-5.)"""
+    gpu, ref, off = run_case(1, 900, 4, 2, 128, dtype, offsets=[0, 200, 201, 555, 900], seed=41, offload="qkvol",
+                             poison=True, softmax_scale=scale)
+    check_all(gpu, ref, dtype, off)

@@ -21,13 +21,14 @@ def announce(msg):
     print(f"\n[case] {msg}", file=sys.stderr, flush=True)
 
 
-def walk_both(B, S, Hq, Hkv, D, dtype, offsets, seed):
+def walk_both(B, S, Hq, Hkv, D, dtype, offsets, seed, scale=0.0):
     """dq, dk, dv of the reverse walk N-1..0 with the context's backward and
-    with the allocation-free one (chunk N-1 overwrites dK/dV, the rest add)."""
-    announce(f"no-alloc walk B={B} S={S} Hq={Hq} Hkv={Hkv} D={D} {dtype} offsets={offsets}")
+    with the allocation-free one (chunk N-1 overwrites dK/dV, the rest add);
+    scale 0 is 1/sqrt(D)."""
+    announce(f"no-alloc walk B={B} S={S} Hq={Hq} Hkv={Hkv} D={D} {dtype} offsets={offsets} scale={scale}")
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     inp = make_inputs(B, S, Hq, Hkv, D, tdt, seed=seed, device="cuda")
-    ca = ChunkedAttention(B, S, len(offsets) - 1, Hq, Hkv, D, dtype=dtype, offsets=offsets)
+    ca = ChunkedAttention(B, S, len(offsets) - 1, Hq, Hkv, D, dtype=dtype, offsets=offsets, scale=scale)
     N = ca.N
     out = ca.alloc_outputs()
     qc = [ca.chunk_view(inp["q"], i) for i in range(N)]
@@ -47,7 +48,7 @@ def walk_both(B, S, Hq, Hkv, D, dtype, offsets, seed):
                 L.sppo_attn_bwd_chunk(ca.ctx, i, qc[i], inp["k"], inp["v"], oc[i], out["lse"][i], dc[i], dq[i],
                                       dk, dv)
             else:
-                L.sppo_attn_bwd_chunk_noalloc(B, S, ca.offsets[i], ca.offsets[i + 1], Hq, Hkv, D, dtype, 0.0,
+                L.sppo_attn_bwd_chunk_noalloc(B, S, ca.offsets[i], ca.offsets[i + 1], Hq, Hkv, D, dtype, scale,
                                               0 if i == N - 1 else 1, qc[i], inp["k"], inp["v"], oc[i],
                                               out["lse"][i], dc[i], dq[i], dk, dv)
         torch.cuda.synchronize()
@@ -61,12 +62,15 @@ def walk_both(B, S, Hq, Hkv, D, dtype, offsets, seed):
 def test_noalloc_backward_matches_the_context_backward(dtype):
     big = walk_both(1, 4096, 8, 2, 128, dtype, [0, 1024, 2048, 3072, 4096], seed=31)
     small = walk_both(2, 1000, 2, 1, 64, dtype, [0, 77, 300, 301, 1000], seed=32)
-    for res in (big, small):
+    scaled = walk_both(2, 1000, 2, 1, 64, dtype, [0, 77, 300, 301, 1000], seed=32, scale=0.15)
+    for res in (big, small, scaled):
         (dq_a, dk_a, dv_a), (dq_b, dk_b, dv_b) = res["ctx"], res["noalloc"]
         for a, b in zip(dq_a, dq_b):
             assert torch.equal(a, b)
         assert torch.equal(dk_a, dk_b) and torch.equal(dv_a, dv_b)
         assert torch.isfinite(dk_b).all()
+    # the explicit scale reached the kernels (the walks differ only in it)
+    assert not torch.equal(small["noalloc"][1], scaled["noalloc"][1])
 
 
 def test_noalloc_rejects_a_chunk_beyond_the_workspace():

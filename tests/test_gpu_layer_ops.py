@@ -125,3 +125,37 @@ def test_gelu_and_pack():
     torch.cuda.synchronize()
     ref = torch.cat([dq, dk[c0:c0 + rows].to(bf), dv[c0:c0 + rows].to(bf)], dim=1)
     assert torch.equal(out.cpu(), ref)
+
+
+def test_layernorm_epsilon_reaches_the_kernel():
+    """Rows of small variance (std 0.02) with eps = 1e-3 against the oracle's
+    LayerNorm at the same eps: there 1/sqrt(var + eps) is 27% below
+    1/sqrt(var), so a kernel that kept its own eps would miss by far more
+    than the gate."""
+    rows, H = 9, 256
+    announce(f"layernorm eps rows={rows} H={H}")
+    g = torch.Generator().manual_seed(5)
+    x = (0.02 * torch.randn(rows, H, generator=g) + 0.3).to(bf)
+    dy = torch.randn(rows, H, generator=g).to(bf)
+    gamma, beta = 1 + 0.1 * torch.randn(H, generator=g), 0.1 * torch.randn(H, generator=g)
+    eps = 1e-3
+    y = torch.empty(rows, H, device="cuda", dtype=bf)
+    mean, rstd = torch.empty(rows, device="cuda"), torch.empty(rows, device="cuda")
+    xd, gd = x.cuda(), gamma.cuda()
+    L.sppo_layernorm_fwd(rows, H, xd, H, gd, beta.cuda(), eps, y, H, mean, rstd, stream=stream())
+    ws_bytes = L.sppo_layernorm_bwd_workspace(rows, H)
+    ws = torch.empty(ws_bytes // 4, device="cuda")
+    dx = torch.empty(rows, H, device="cuda", dtype=bf)
+    zeros = torch.zeros(rows, H, device="cuda", dtype=bf)
+    dg, db = torch.empty(H, device="cuda"), torch.empty(H, device="cuda")
+    L.sppo_layernorm_bwd(rows, H, xd, H, gd, mean, rstd, dy.cuda(), H, zeros, H, dx, H, dg, db, ws, ws_bytes,
+                         accumulate=0, stream=stream())
+    torch.cuda.synchronize()
+    xh = to_np(x)
+    ref_y, ref_m, ref_r = T.layer_norm(xh, to_np(gamma), to_np(beta), eps=eps)
+    assert np.abs(1 / np.sqrt(xh.var(axis=1) + eps) * np.sqrt(xh.var(axis=1)) - 1).min() > 0.2  # eps matters
+    np.testing.assert_allclose(to_np(rstd), ref_r, rtol=1e-4)
+    assert np.abs(to_np(y) - ref_y).max() <= 8e-3 * np.abs(ref_y).max()
+    ref_dx, ref_dg, ref_db = T.layer_norm_bwd(xh, to_np(gamma), ref_m, ref_r, to_np(dy))
+    assert np.abs(to_np(dx) - ref_dx).max() <= 1e-2 * np.abs(ref_dx).max()
+    np.testing.assert_allclose(to_np(dg), ref_dg, rtol=2e-4, atol=2e-4 * np.abs(ref_dg).max())

@@ -24,7 +24,7 @@ def announce(msg):
 
 
 def run_case(B, S, Hq, Hkv, D, dtype, N=None, offsets=None, seed=0, kind="randn",
-             offload="none", lookahead=2, poison=False, rows=None, softmax_scale=None):
+             offload="none", lookahead=2, poison=False, rows=None, softmax_scale=None, fwd_slots=4):
     if offsets is None:
         offsets = list(oracle.equal_offsets(S, N))
     N = len(offsets) - 1
@@ -33,7 +33,7 @@ def run_case(B, S, Hq, Hkv, D, dtype, N=None, offsets=None, seed=0, kind="randn"
     inp = make_inputs(B, S, Hq, Hkv, D, TORCH_DT[dtype], seed=seed, device="cuda", kind=kind)
     host = {n: to_np(t) for n, t in inp.items()}  # taken before the HIP path runs
     ca = ChunkedAttention(B, S, N, Hq, Hkv, D, dtype=dtype, offsets=offsets, offload=offload,
-                          scale=softmax_scale or 0.0)
+                          scale=softmax_scale or 0.0, fwd_slots=fwd_slots)
     if rows is not None:
         ca.set_offload_rows(rows)
     out = ca.alloc_outputs()
@@ -224,3 +224,15 @@ def test_explicit_softmax_scale(dtype, scale):
     gpu, ref, off = run_case(1, 900, 4, 2, 128, dtype, offsets=[0, 200, 201, 555, 900], seed=41, offload="qkvol",
                              poison=True, softmax_scale=scale)
     check_all(gpu, ref, dtype, off)
+
+
+@pytest.mark.parametrize("fwd_slots,lookahead", [(1, 0), (1, 2), (2, 1)])
+def test_tight_arena(fwd_slots, lookahead):
+    """The smallest device arenas: with fwd_slots = 1 every forward chunk
+    reuses the region of the chunk just offloaded (the compute stream waits
+    for that copy first), with 2 the one before it; the backward's prefetch
+    reuses regions as they free up.  Ragged GQA chunks, offloaded and
+    poisoned."""
+    gpu, ref, off = run_case(1, 1500, 4, 2, 128, "bf16", offsets=[0, 300, 301, 700, 1100, 1500], seed=43,
+                             offload="qkvol", poison=True, fwd_slots=fwd_slots, lookahead=lookahead)
+    check_all(gpu, ref, "bf16", off)

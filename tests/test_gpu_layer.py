@@ -35,14 +35,14 @@ def announce(msg):
     print(f"\n[case] {msg}", file=sys.stderr, flush=True)
 
 
-def run_layer(S, Hq, Hkv, D, offsets, seed=0, offload="none", poison=False, lookahead=2, rows=None):
+def run_layer(S, Hq, Hkv, D, offsets, seed=0, offload="none", poison=False, lookahead=2, rows=None, fwd_slots=4):
     announce(f"layer S={S} Hq={Hq} Hkv={Hkv} D={D} offsets={offsets} seed={seed} offload={offload} "
              f"poison={poison} rows={rows}")
     inp, p = make_layer_inputs(S, Hq, Hkv, D, seed, device="cpu")
     host = {k: to_np(v) for k, v in {**inp, **p}.items()}
     dinp = {k: v.cuda() for k, v in inp.items()}
     dp = {k: v.cuda() for k, v in p.items()}
-    lay = ChunkedLayer(S, len(offsets) - 1, Hq, Hkv, D, offsets=offsets, offload=offload)
+    lay = ChunkedLayer(S, len(offsets) - 1, Hq, Hkv, D, offsets=offsets, offload=offload, fwd_slots=fwd_slots)
     if rows is not None:
         lay.set_offload_rows(rows)
     out = lay.alloc_outputs()
@@ -89,6 +89,18 @@ def test_layer_offload_is_bitwise_invisible(offload, rows):
         rows = [min(r, offsets[i + 1] - offsets[i]) for i, r in enumerate(rows)]
     base, host = run_layer(1024, 2, 2, 128, offsets, seed=2)
     got, _ = run_layer(1024, 2, 2, 128, offsets, seed=2, offload=offload, poison=True, lookahead=1, rows=rows)
+    for k in KEYS:
+        assert np.array_equal(got[k], base[k]), k
+
+
+def test_layer_tight_arena_is_bitwise_invisible():
+    """The smallest arena (fwd_slots 1: each forward chunk reuses the region
+    of the chunk just offloaded, after its copy) with lookahead 0, K/V
+    evicted, everything dead poisoned."""
+    offsets = [0, 200, 201, 600, 1024]
+    base, _ = run_layer(1024, 2, 2, 128, offsets, seed=4)
+    got, _ = run_layer(1024, 2, 2, 128, offsets, seed=4, offload="qkvol_evict", poison=True, lookahead=0,
+                       fwd_slots=1)
     for k in KEYS:
         assert np.array_equal(got[k], base[k]), k
 

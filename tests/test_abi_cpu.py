@@ -1,6 +1,8 @@
 """The C-ABI library loads, exports every entry point include/sppo.h
-declares, and rejects invalid problems before touching the GPU (CPU only)."""
+declares, and rejects invalid problems before touching the GPU (CPU only);
+the public headers compile as C and C++."""
 import ctypes
+import os
 
 import pytest
 
@@ -140,3 +142,23 @@ def test_noalloc_backward_checks_arguments_on_the_host(change, status):
                                       a["acc"], *p, stream=0)
     assert ei.value.status == status
     assert L.sppo_last_error(None)
+
+
+def test_headers_compile_as_c99_and_cxx(tmp_path):
+    """Every public header is valid C (C99, warnings as errors) and C++: a C
+    caller gets the same declarations through extern "C"."""
+    import glob
+    import shutil
+    import subprocess
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    heads = sorted(os.path.basename(h) for h in glob.glob(os.path.join(inc, "*.h")))
+    assert heads
+    src = "".join(f'#include "{h}"\n' for h in heads) + "int main(void) { return 0; }\n"
+    for cc, ext, std in (("gcc", "c", "-std=c99"), ("g++", "cpp", "-std=c++17")):
+        if shutil.which(cc) is None:
+            pytest.skip(f"{cc} not available")
+        f = tmp_path / f"h.{ext}"
+        f.write_text(src)
+        r = subprocess.run([cc, std, "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", inc, "-c", str(f),
+                            "-o", str(tmp_path / f"h_{ext}.o")], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr

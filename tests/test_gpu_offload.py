@@ -508,3 +508,50 @@ def test_contexts_on_two_streams_run_concurrently():
         got = {"o": out["o"], "lse": ca.lse_full(out), "dq": out["dq"], "dk": out["dk"], "dv": out["dv"]}
         assert_bitwise(ref, got)
         ca.close()
+
+
+def test_contexts_from_two_host_threads():
+    """Two host threads each create a context, run an offloading walk with
+    poison on a stream of their own and destroy it, twice over (the library
+    calls release the interpreter lock, so creation, the shared copy
+    streams' reference counts, the walks and destruction interleave): every
+    walk gives the bits of the same walk run alone."""
+    import threading
+
+    seeds, modes = (51, 52), ("qkvol", "qkvol_evict")
+    refs = [run(m, seed=sd)[0] for m, sd in zip(modes, seeds)]
+    announce("two host threads, two contexts each")
+    S, Hq, Hkv, D = SHAPE["S"], SHAPE["Hq"], SHAPE["Hkv"], SHAPE["D"]
+    inps = [make_inputs(1, S, Hq, Hkv, D, torch.bfloat16, seed=sd, device="cuda") for sd in seeds]
+    torch.cuda.synchronize()
+    results, errors = [[], []], []
+
+    def worker(t):
+        try:
+            torch.cuda.set_device(0)
+            st = torch.cuda.Stream()
+            for _ in range(2):
+                with torch.cuda.stream(st):
+                    ca = ChunkedAttention(1, S, N, Hq, Hkv, D, dtype="bf16", offload=modes[t], host_ahead=1)
+                    out = ca.alloc_outputs()
+                    inp = {n: x.clone() for n, x in inps[t].items()}  # poison overwrites the offloaded rows of q
+                    ca.step(inp, out, poison=True, stream=st)
+                    st.synchronize()
+                    results[t].append({"o": out["o"].clone(), "lse": ca.lse_full(out).clone(),
+                                       "dq": out["dq"].clone(), "dk": out["dk"].clone(), "dv": out["dv"].clone()})
+                    st.synchronize()
+                    ca.close()
+        except Exception as e:  # reported by the main thread
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=worker, args=(t,)) for t in range(2)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join(timeout=90)
+    assert not any(th.is_alive() for th in threads), "a worker did not finish"
+    assert not errors, errors
+    for t in range(2):
+        assert len(results[t]) == 2
+        for got in results[t]:
+            assert_bitwise(refs[t], got)

@@ -344,10 +344,11 @@ sppo_status sppo_prefetch_wait(sppo_ctx* ctx, int32_t i, void* stream);
  * allocation.  Its Delta / LSE workspace and the dK/dV kernel's tile
  * queues are a static device array of the library (8 MiB on every GPU the
  * library runs on, held until the process ends; the queues are cleared by
- * each call and left zero), so batch * n_q_heads * (c1 - c0) must not exceed 2^20
- * (UNSUPPORTED otherwise, as for the size limits of sppo_create).  Every call on one GPU shares that GPU's array:
- * calls that overlap on one GPU (several streams or threads) race, so the
- * caller orders them (e.g. one stream).  Arguments as in sppo_create and
+ * each call and left zero), so batch * n_q_heads * (c1 - c0) must not
+ * exceed 2^20 (UNSUPPORTED otherwise, as for the size limits of
+ * sppo_create).  Every call on one GPU shares that GPU's array: calls that
+ * overlap on one GPU (several streams or threads) race, so the caller
+ * orders them (e.g. one stream).  Arguments as in sppo_create and
  * sppo_attn_bwd_chunk: q_i, o_i, do_i, dq_i [B, c1 - c0, Hq, D] and lse_i
  * [B, Hq, c1 - c0] chunk-local; k, v [B, S, Hkv, D]; dk_acc, dv_acc fp32
  * [B, S, Hkv, D], rows [0, c1) overwritten (accumulate = 0) or added to
